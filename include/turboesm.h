@@ -1,0 +1,216 @@
+/*
+ * turboesm.h -- C ABI of the TurboESM 3-bit KV-cache quantizer and fused
+ * decode attention for MI355X (gfx950).
+ *
+ * The method (TurboESM, arXiv 2603.26110) stores the key/value cache of a
+ * rotary-position-embedding (RoPE) transformer in 3-bit codes:
+ *   prefill  (Sec. 3.1, "operational pipeline", steps 1, 3, 4):
+ *       k' = R_{theta,p} k           RoPE first (Eq. 1-2)
+ *       k^ = Pi k'                    per-head orthogonal rotation (Eq. 4)
+ *       3-bit Lloyd-Max codes of k^   separate K and V tables (Sec. 3.3, Eq. 5)
+ *       1-bit QJL residual signs      (Sec. 3.4, Eq. 6-7)
+ *   decode   (Sec. 3.1 decode steps 1-4, Algorithm 1 of Sec. 4.3):
+ *       one pass over the packed cache: dequantize through the tables in
+ *       registers, add the QJL score correction, online softmax, accumulate V.
+ *
+ * Every entry point is asynchronous on the HIP stream it is given and never
+ * synchronizes. Device pointers are plain device addresses (hipMalloc or
+ * torch allocations on the current device). The library allocates no device
+ * memory: the caller owns every buffer, including the cache and workspace.
+ * Errors detected on the host are reported before anything is launched:
+ * the call returns a negative tq_status and tq_last_error() returns a
+ * thread-local message. Device code never traps; per-sequence metadata held
+ * in device memory is checked by the kernels, which skip what is out of range
+ * as documented per entry point.
+ *
+ * Fixed layout facts (head_dim must be 64):
+ *   - code words: a token-head vector of 64 codes is 32 bytes; code i is the
+ *     nibble at bits 4*(i%8) .. 4*(i%8)+3 of 32-bit word i/8 (little endian).
+ *     Nibble = idx | (sign << 3): idx is the 3-bit LUT index, sign the QJL bit
+ *     (K always; V only with TQ_V_QJL, else 0).
+ *   - tile interleaving: slots are grouped in tiles of 64. For slot s of a
+ *     (layer, head) region, tile t = s/64, lane r = s%64, the 16-byte half c
+ *     (c = 0: words 0-3, c = 1: words 4-7) lives at byte
+ *         region_base + t*2048 + (c*64 + r)*16
+ *     in k_codes (and likewise v_codes), region_base = (l*H + h)*slots*32.
+ *   - scalars: 4 fp16 values per slot at byte (l*H + h)*slots*8 + s*8:
+ *         [0] n_k  = ||k^||,  [1] g_k = ||r_k|| (QJL residual norm),
+ *         [2] n_v  = ||v^||,  [3] g_v = ||r_v|| (0 unless TQ_V_QJL).
+ *   That is 72 bytes per cached token-head (4.5 bits per element).
+ */
+#ifndef TURBOESM_H
+#define TURBOESM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+typedef int32_t tq_status;
+#define TQ_OK             0
+#define TQ_ERR_ARG       -1  /* null pointer, bad count or unknown flag      */
+#define TQ_ERR_DIM       -2  /* head_dim != 64 or layer range outside [0, L) */
+#define TQ_ERR_ALIGN     -3  /* a pointer misses its documented alignment    */
+#define TQ_ERR_CAPACITY  -5  /* slots not a positive multiple of 64, or a
+                                workspace smaller than required              */
+#define TQ_ERR_HIP       -6  /* a HIP runtime call or kernel launch failed   */
+
+/* ---- element types of k, v, q and out ---------------------------------- */
+#define TQ_F32 0
+#define TQ_F16 1
+
+/* ---- behaviour flags (tq_params.flags) ----------------------------------
+ * TQ_V_ROTATE      V is stored in the rotated basis v^ = Pi v and decode
+ *                  applies one inverse rotation Pi^T to the attention
+ *                  output. Without it V is quantized unrotated (Sec. 3.3:
+ *                  the value table is calibrated on unrotated values).
+ * TQ_V_QJL         V also carries QJL sign bits and a residual norm, and
+ *                  decode adds the V residual estimate (Algorithm 1 corrects
+ *                  both K and V).
+ * TQ_QJL_PAPER     residual signs are taken per element, s_i = sign(r_i),
+ *                  and decode adds s_i * ebar with the per-head mean absolute
+ *                  residual ebar (Sec. 3.4, Eq. 6-7) instead of the projected
+ *                  estimator. Requires `ebar`.
+ * TQ_ROPE_HALF     RoPE pairs dimensions (m, m+32) instead of (2m, 2m+1).
+ * TQ_INPUT_ROTATED quantize inputs are already x^ (fp32): RoPE and Pi are
+ *                  skipped. Used to check the codes bit for bit.
+ * TQ_OUT_FP32      decode writes fp32 output even when io_dtype is TQ_F16.
+ */
+#define TQ_V_ROTATE      (1u << 0)
+#define TQ_V_QJL         (1u << 1)
+#define TQ_QJL_PAPER     (1u << 2)
+#define TQ_ROPE_HALF     (1u << 3)
+#define TQ_INPUT_ROTATED (1u << 4)
+#define TQ_OUT_FP32      (1u << 5)
+#define TQ_FLAGS_ALL     0x3Fu
+
+/* Model-level parameters shared by every call on one cache. */
+typedef struct tq_params {
+  int32_t head_dim;        /* must be 64                                      */
+  int32_t num_layers;      /* L: layers of the cache and of pi / lut arrays   */
+  int32_t num_heads;       /* H                                               */
+  int32_t io_dtype;        /* TQ_F16 or TQ_F32 for k, v, q and out            */
+  uint32_t flags;          /* TQ_* flags above                                */
+  float softmax_scale;     /* logit = score * softmax_scale; <= 0 means 1/8   */
+  const float* rope_cs;    /* device [rope_positions][32][2] (cos, sin) from
+                              tq_rope_table; 8-byte aligned                  */
+  int32_t rope_positions;  /* rows of rope_cs; positions must be below it     */
+} tq_params;
+
+/* The packed cache. Every (layer, head) owns `slots` consecutive slots. */
+typedef struct tq_cache {
+  void* k_codes;           /* device, L*H*slots*32 bytes, 16-byte aligned     */
+  void* v_codes;           /* device, L*H*slots*32 bytes, 16-byte aligned     */
+  void* scalars;           /* device, L*H*slots*8 bytes,  8-byte aligned      */
+  int64_t slots;           /* slots per (layer, head), positive multiple of 64 */
+} tq_cache;
+
+/* Bytes of k_codes + v_codes + scalars for a cache of L x H x slots
+ * (72 bytes per slot per head; the memory accounting of Table 4 in Sec. 5.2
+ * counts the same 3-bit codes in 4-bit containers plus 1-bit K signs).
+ * Returns -1 for negative arguments. */
+int64_t tq_cache_bytes(int32_t num_layers, int32_t num_heads, int64_t slots);
+
+/* RoPE cos/sin table (Eq. 2). For position p < positions and pair m < 32:
+ *   theta_m = base^(-2m/64),  a = p * theta_m  (both in double precision),
+ *   cs[(p*32 + m)*2 + 0] = (float)cos(a),  cs[(p*32 + m)*2 + 1] = (float)sin(a).
+ * cs: device, positions*64 floats, 8-byte aligned. base > 0 (10000 for ESM-2). */
+tq_status tq_rope_table(float* cs, int32_t positions, double base, void* stream);
+
+/* Prefill-side quantizer (Sec. 3.1 prefill steps 1, 3, 4; Sec. 3.3; Sec. 3.4;
+ * Sec. 4.2). For every layer l in [layer0, layer0+nlayers), sequence b < B,
+ * token j < T and head h < H:
+ *   k' = RoPE(k, pos0[b] + j)                          (skipped: TQ_INPUT_ROTATED)
+ *   k^ = Pi_{l,h} k'          v^ = Pi_{l,h} v (TQ_V_ROTATE) or v
+ *   for x^ in {k^, v^} with its table c (lut_k or lut_v), all in binary32:
+ *     n  = sqrt(fma-chain sum_i x^_i^2, i ascending);  inv = n > 0 ? 8/n : 0
+ *     u_i = x^_i * inv;   t_m = 0.5*(c_m + c_{m+1});   idx_i = #{m : u_i > t_m}
+ *     r_i = u_i - c[idx_i];  g = sqrt(fma-chain sum_i r_i^2)
+ *     sign_i = !(p_i < 0), p_i = fma-chain sum_k S[i][k] r_k   (K; V with TQ_V_QJL)
+ *            = !(r_i < 0)                                       (TQ_QJL_PAPER)
+ *     n, g stored as fp16 (round to nearest even, saturated at 65504)
+ *   and writes codes and scalars to slot slot0[b] + j of region (l, h).
+ * Codes are bit-identical to a sequential binary32 evaluation of the above
+ * whenever x^ is the same (TQ_INPUT_ROTATED makes x^ an input).
+ *
+ *   k, v   device [nlayers][B][T][H][64] of io_dtype (fp32 when
+ *          TQ_INPUT_ROTATED); 16-byte aligned. Layer index is relative to layer0.
+ *   pos0   device int32 [B]: RoPE position of token 0 of each sequence.
+ *   slot0  device int64 [B]: cache slot of token 0 of each sequence.
+ *          Tokens whose slot falls outside [0, slots) or whose position
+ *          falls outside [0, rope_positions) are not written.
+ *   pi     device [L][H][64][64] fp32, row-major, x^ = pi . x (absolute layer).
+ *   lut_k, lut_v  device [L][H][8] fp32, strictly ascending.
+ *   qjl_s  device [64][64] fp32 Gaussian projection S (ignored with TQ_QJL_PAPER).
+ *   ebar   unused by the quantizer (may be NULL).
+ */
+tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache,
+                           const void* k, const void* v,
+                           int32_t B, int32_t T, int32_t layer0, int32_t nlayers,
+                           const int32_t* pos0, const int64_t* slot0,
+                           const float* pi, const float* lut_k, const float* lut_v,
+                           const float* qjl_s, const float* ebar, void* stream);
+
+/* Fused decode attention over the packed cache (Sec. 3.1 decode steps 1-4;
+ * Algorithm 1 of Sec. 4.3; the query is rotated once instead of rotating
+ * every key, which Eq. 4 makes identical). For every layer l in
+ * [layer0, layer0+nlayers), sequence b and head h, with n = seq_len[b]
+ * cached tokens in slots seq_slot0[b] .. seq_slot0[b]+n-1:
+ *   q^ = Pi RoPE(q, q_pos[b]);   u = S q^;   alpha = sqrt(pi/2)/64
+ *   score_j = (n_k,j/8) * ( sum_i q^_i c_K[idx_ij] + alpha g_k,j sum_i u_i (2 s_ij - 1) )
+ *             (TQ_QJL_PAPER: alpha g_k,j -> ebar_K and u -> q^)
+ *   w_j = exp(score_j * softmax_scale - max);   o^ = sum_j w_j v~_j / sum_j w_j
+ *   v~_j = (n_v,j/8) * ( c_V[idx^V_j] (+ V residual estimate with TQ_V_QJL) )
+ *   out = Pi^T o^ (TQ_V_ROTATE) or o^.   n = 0 gives out = 0.
+ *
+ *   q       device [nlayers][B][H][64] io_dtype, before RoPE; 16-byte aligned.
+ *   q_pos   device int32 [B]: RoPE position of the query.
+ *   seq_slot0 device int64 [B]: first slot of each sequence, multiple of 64.
+ *   seq_len device int32 [B]: cached tokens, 0 <= seq_len <= max_len.
+ *           A sequence whose range or query position is invalid gets NaN output.
+ *   max_len host bound on every seq_len (sizes the split-K grid), >= 0.
+ *   out     device [nlayers][B][H][64]: io_dtype, or fp32 with TQ_OUT_FP32.
+ *   workspace device, >= tq_decode_workspace_bytes(...) bytes, 16-byte aligned
+ *           (may be NULL when that is 0). It must be zero-filled before its
+ *           first use; every call leaves it zero-filled again.
+ *           Calls that share a workspace must be ordered on one stream.
+ */
+tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache,
+                           const void* q, int32_t B, int32_t layer0, int32_t nlayers,
+                           const int32_t* q_pos, const int64_t* seq_slot0,
+                           const int32_t* seq_len, int32_t max_len,
+                           const float* pi, const float* lut_k, const float* lut_v,
+                           const float* qjl_s, const float* ebar,
+                           void* out, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* Workspace bytes tq_decode_attend needs for these sizes (0 if none). */
+size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B,
+                                 int32_t nlayers, int32_t max_len);
+
+/* Head-wise rotation calibration (Sec. 3.2): for each head, X is the
+ * [ncal][64] matrix of post-RoPE keys, X = U Sigma V^T, Pi = V^T.
+ * Computed as the eigen-decomposition of the fp64 Gram matrix X^T X (cyclic
+ * Jacobi, fp64), rows ordered by descending singular value, each row's
+ * entry of largest magnitude made positive (lowest index on ties).
+ *   x        device [nheads][ncal][64] fp32 (not centered).
+ *   pi_out   device [nheads][64][64] fp32.
+ *   sing_out device [nheads][64] fp32 singular values, or NULL.
+ */
+tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal,
+                                float* pi_out, float* sing_out, void* stream);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char* tq_last_error(void);
+
+/* Library version string. */
+const char* tq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TURBOESM_H */

@@ -1,0 +1,251 @@
+"""Pins of the oracle's quantizer (Sec. 3.3, Eq. 5; Sec. 3.4, Eq. 6) and cache
+packing (Sec. 4.2): library routines, fp64 recomputation away from decision
+boundaries, hand-worked cases and brute force."""
+import numpy as np
+import pytest
+
+from oracle import oracle
+from paper_2603_26110_amd import synth
+
+LUT, _, _ = oracle.lloyd_max_gaussian(8)
+LUT32 = LUT.astype(np.float32)
+
+
+# ---------------------------------------------------------------- fp16 storage
+def test_fp16_conversion_matches_numpy():
+    g = synth.rng(1)
+    vals = np.concatenate([
+        g.standard_normal(3000).astype(np.float32) * np.float32(100),
+        g.standard_normal(1000).astype(np.float32) * np.float32(1e-5),    # subnormal range
+        np.array([0.0, -0.0, 1.0, 65504.0, 65519.0, 65520.0, 1e6, -1e6, 2.0 ** -24,
+                  2.0 ** -25, 2.0 ** -25 * 1.0001, 2.0 ** -14, 2.0 ** -14 * (1 - 2 ** -12),
+                  1.0 + 2.0 ** -11, 1.0 + 3 * 2.0 ** -11, np.inf, -np.inf], dtype=np.float32),
+    ])
+    got = oracle.f32_to_f16_bits(vals)
+    ref = vals.astype(np.float16).view(np.uint16)
+    np.testing.assert_array_equal(got, ref)
+    back = oracle.f16_bits_to_f32(ref)
+    np.testing.assert_array_equal(back, ref.view(np.float16).astype(np.float32))
+    assert oracle.f32_to_f16_bits(np.array([np.nan], np.float32))[0] & 0x7C00 == 0x7C00
+
+
+# -------------------------------------------------------------- quantize rules
+def _unpack(nib):
+    return (nib & 7).astype(np.int64), (nib >> 3).astype(np.int64)
+
+
+def test_codes_are_nearest_levels_and_norms_match_fp64():
+    g = synth.rng(2)
+    S = synth.qjl_matrix(g)
+    t64 = 0.5 * (LUT32[:-1].astype(np.float64) + LUT32[1:])
+    near = 0
+    for _ in range(300):
+        x = (g.standard_normal(64) * g.uniform(0.1, 30)).astype(np.float32)
+        nib, n16, g16 = oracle.quantize_vector(x, LUT32, S)
+        idx, _ = _unpack(nib)
+        n = np.linalg.norm(x.astype(np.float64))
+        u = x.astype(np.float64) * 8.0 / n
+        ref = oracle.assign_levels(u, LUT32.astype(np.float64))
+        close = np.min(np.abs(u[:, None] - t64[None, :]), axis=1) < 1e-5
+        near += int(close.sum())
+        np.testing.assert_array_equal(idx[~close], ref[~close])
+        # stored norm: fp16 of ||x||
+        assert abs(np.float16(np.uint16(n16).view(np.float16)) - n) <= 2.0 ** -10 * n
+        r = u - LUT32[idx].astype(np.float64)
+        gam = np.linalg.norm(r)
+        assert abs(float(np.uint16(g16).view(np.float16)) - gam) <= 2.0 ** -10 * gam + 1e-6
+    assert near < 50
+
+
+def test_projected_sign_bits_match_fp64_away_from_zero():
+    g = synth.rng(3)
+    S = synth.qjl_matrix(g)
+    checked = 0
+    for _ in range(200):
+        x = g.standard_normal(64).astype(np.float32)
+        nib, _, _ = oracle.quantize_vector(x, LUT32, S, oracle.SIGN_PROJECTED)
+        idx, sgn = _unpack(nib)
+        u = x.astype(np.float64) * 8.0 / np.linalg.norm(x.astype(np.float64))
+        r = u - LUT32[idx]
+        p = S.astype(np.float64) @ r
+        bound = 1e-4 * np.linalg.norm(S, axis=1) * np.linalg.norm(r)
+        ok = np.abs(p) > bound
+        np.testing.assert_array_equal(sgn[ok], (p[ok] >= 0).astype(np.int64))
+        checked += int(ok.sum())
+    assert checked > 200 * 60
+
+
+def test_element_sign_bits_are_residual_signs():
+    g = synth.rng(4)
+    S = synth.qjl_matrix(g)
+    for _ in range(100):
+        x = g.standard_normal(64).astype(np.float32)
+        nib, _, g16 = oracle.quantize_vector(x, LUT32, S, oracle.SIGN_ELEMENT)
+        idx, sgn = _unpack(nib)
+        u = x.astype(np.float64) * 8.0 / np.linalg.norm(x.astype(np.float64))
+        r = u - LUT32[idx]
+        ok = np.abs(r) > 1e-5
+        np.testing.assert_array_equal(sgn[ok], (r[ok] >= 0).astype(np.int64))
+        assert g16 != 0
+
+
+def test_no_sign_mode_stores_zero_bits_and_zero_residual_norm():
+    x = synth.rng(5).standard_normal(64).astype(np.float32)
+    nib, _, g16 = oracle.quantize_vector(x, LUT32, np.eye(64, dtype=np.float32), oracle.SIGN_NONE)
+    assert np.all(nib >> 3 == 0) and g16 == 0
+
+
+def test_hand_worked_constant_vector():
+    # x = a * (1, ..., 1): n = 8a, u_i = 1 exactly; Gaussian levels put 1.0
+    # between thresholds 0.5006 and 1.0500 -> index 5 (level 0.7560);
+    # r_i = 1 - 0.7560 > 0 -> every element sign is 1; g = 8 * (1 - c5).
+    x = np.full(64, 0.75, dtype=np.float32)
+    nib, n16, g16 = oracle.quantize_vector(x, LUT32, np.eye(64, dtype=np.float32), oracle.SIGN_PROJECTED)
+    assert np.all(nib == (5 | 8))
+    assert n16 == np.float16(6.0).view(np.uint16)
+    assert abs(float(np.uint16(g16).view(np.float16)) - 8 * (1 - LUT[5])) < 2e-3
+
+
+def test_zero_vector():
+    # n = 0 -> u = 0; the symmetric table has t_3 = 0 exactly and 0 > 0 is
+    # false -> index 3; r = -c_3 > 0; with S = I every sign is 1.
+    nib, n16, g16 = oracle.quantize_vector(np.zeros(64, np.float32), LUT32,
+                                          np.eye(64, dtype=np.float32))
+    assert np.all(nib == (3 | 8)) and n16 == 0
+    assert abs(float(np.uint16(g16).view(np.float16)) + 8 * LUT[3]) < 2e-3
+
+
+def test_threshold_ties_go_to_the_lower_level_and_zero_residual_sign_is_plus():
+    # Levels 0.5 and 1.5 have midpoint 1.0; u = 1 exactly sits on it -> lower level.
+    lut = np.array([-3, -2, -1, 0, 0.5, 1.5, 2.5, 3.5], dtype=np.float32)
+    x = np.full(64, 2.0, dtype=np.float32)                 # u = 1 exactly
+    nib, _, _ = oracle.quantize_vector(x, lut, np.eye(64, dtype=np.float32))
+    assert np.all((nib & 7) == 4)
+    # a level exactly at u = 1 -> r = 0 -> sign(0) = +1, g = 0
+    lut2 = np.array([-3, -2, -1, 0, 0.5, 1.0, 2.5, 3.5], dtype=np.float32)
+    nib, _, g16 = oracle.quantize_vector(x, lut2, np.eye(64, dtype=np.float32))
+    assert np.all(nib == (5 | 8)) and g16 == 0
+    nib, _, _ = oracle.quantize_vector(x, lut2, np.eye(64, dtype=np.float32), oracle.SIGN_ELEMENT)
+    assert np.all(nib == (5 | 8))
+
+
+def test_norm_saturates_at_fp16_max():
+    x = np.full(64, 20000.0, dtype=np.float32)             # ||x|| = 160000
+    _, n16, _ = oracle.quantize_vector(x, LUT32, np.eye(64, dtype=np.float32))
+    assert n16 == 0x7BFF                                   # 65504
+
+
+def test_brute_force_index_on_small_grid():
+    # Every u on a fine grid: the threshold count equals the nearest level
+    # with ties low (brute force over the 8 levels).
+    lut = LUT32
+    grid = np.linspace(-3, 3, 64 * 20).astype(np.float32).reshape(20, 64)
+    for row in grid:
+        # choose x so that u = row * 8 / ||row||: just quantize row itself
+        nib, _, _ = oracle.quantize_vector(row, lut, np.eye(64, dtype=np.float32))
+        n = np.float32(np.sqrt(np.sum(row.astype(np.float64) ** 2)))
+        u = row.astype(np.float64) * 8.0 / n
+        d = np.abs(u[:, None] - lut[None, :].astype(np.float64))
+        brute = np.array([np.flatnonzero(r == r.min())[0] for r in d])
+        t64 = 0.5 * (lut[:-1].astype(np.float64) + lut[1:])
+        close = np.min(np.abs(u[:, None] - t64[None, :]), axis=1) < 1e-5
+        np.testing.assert_array_equal((nib & 7)[~close], brute[~close])
+
+
+# ------------------------------------------------------------------ packing
+def test_pack_layout_hand_worked():
+    # Slot 65 = tile 1, lane 1. Nibble 9 = word 1, bits 4..7. Word 1 is in the
+    # first 16-byte half, bytes 4..7 of it; that half sits at
+    # 1*2048 + (0*64 + 1)*16 = 2064. So byte 2064 + 4 + 0 holds 0xA0.
+    region = np.zeros(4096, np.uint8)
+    nib = np.zeros(64, np.uint8)
+    nib[9] = 0xA
+    oracle.pack_slot(region, 65, nib)
+    assert np.flatnonzero(region).tolist() == [2068] and region[2068] == 0xA0
+    # Nibble 63 = word 7 (second half, bytes 12..15), bits 28..31 -> byte 15
+    # of the half at 2048 + (64 + 1)*16 = 3088.
+    region[:] = 0
+    nib[:] = 0
+    nib[63] = 0x7
+    oracle.pack_slot(region, 65, nib)
+    assert np.flatnonzero(region).tolist() == [3088 + 15] and region[3103] == 0x70
+
+
+def test_pack_matches_vectorized_shift_sum_and_round_trips():
+    # Independent construction: 8 nibbles per 32-bit word by a broadcast shift
+    # and sum (the vectorized packing of Sec. 4.2 with 4-bit fields), then
+    # placement of the two 16-byte halves.
+    g = synth.rng(6)
+    slots = 256
+    region = np.zeros(slots * 32, np.uint8)
+    allnib = g.integers(0, 16, (slots, 64)).astype(np.uint8)
+    for s in range(slots):
+        oracle.pack_slot(region, s, allnib[s])
+    words = (allnib.reshape(slots, 8, 8).astype(np.uint32) << (4 * np.arange(8, dtype=np.uint32))).sum(-1)
+    wbytes = words.astype("<u4").view(np.uint8).reshape(slots, 2, 16)
+    ref = np.zeros(slots * 32, np.uint8)
+    for s in range(slots):
+        t, lane = divmod(s, 64)
+        for c in range(2):
+            off = t * 2048 + (c * 64 + lane) * 16
+            ref[off:off + 16] = wbytes[s, c]
+    np.testing.assert_array_equal(region, ref)
+    for s in [0, 1, 63, 64, 200, 255]:
+        np.testing.assert_array_equal(oracle.unpack_slot(region, s), allnib[s])
+
+
+def test_quantize_pack_writes_expected_slots_and_skips_out_of_range():
+    g = synth.rng(7)
+    L, H, B, T = 2, 3, 2, 5
+    cache = oracle.Cache(L, H, 128)
+    cs = oracle.rope_table(64)
+    k = g.standard_normal((1, B, T, H, 64)).astype(np.float32)
+    v = g.standard_normal((1, B, T, H, 64)).astype(np.float32)
+    pi = synth.rotations(g, L, H)
+    S = synth.qjl_matrix(g)
+    luts = np.tile(LUT32, (L, H, 1))
+    pos0 = np.array([3, 60], np.int32)          # sequence 1 runs past position 63 -> skipped
+    slot0 = np.array([0, 124], np.int64)        # sequence 1 runs past slot 127 -> skipped
+    oracle.quantize_pack(cache, oracle.V_ROTATE, cs, k, v, pos0, slot0, pi, luts, luts, S, layer0=1)
+    # layer 0 untouched
+    assert not cache.region("k", 0, 0).any() and not cache.scalars(0, 2).any()
+    for h in range(H):
+        sc = cache.scalars(1, h)
+        # sequence 0: slots 0..4 written; sequence 1: slots 124..127 at positions
+        # 60..63 written, its 5th token (slot 128, position 64) dropped
+        assert np.all(sc[0:5, 0] != 0) and np.all(sc[124:128, 0] != 0)
+        assert not sc[5:124].any()
+        for j in range(T):
+            kh = oracle.rotated_input(k[0, 0, j, h], True, 3 + j, cs, pi[1, h])
+            nib, n16, g16 = oracle.quantize_vector(kh, LUT32, S)
+            np.testing.assert_array_equal(oracle.unpack_slot(cache.region("k", 1, h), j), nib)
+            assert sc[j, 0] == n16 and sc[j, 1] == g16
+            vh = oracle.rotated_input(v[0, 0, j, h], False, 3 + j, cs, pi[1, h])
+            nibv, nv16, gv16 = oracle.quantize_vector(vh, LUT32, S, oracle.SIGN_NONE)
+            np.testing.assert_array_equal(oracle.unpack_slot(cache.region("v", 1, h), j), nibv)
+            assert sc[j, 2] == nv16 and sc[j, 3] == 0
+
+
+@pytest.mark.parametrize("flags,kmode,vmode", [
+    (oracle.V_ROTATE | oracle.V_QJL, oracle.SIGN_PROJECTED, oracle.SIGN_PROJECTED),
+    (oracle.QJL_PAPER, oracle.SIGN_ELEMENT, oracle.SIGN_NONE),
+    (oracle.QJL_PAPER | oracle.V_QJL, oracle.SIGN_ELEMENT, oracle.SIGN_ELEMENT),
+])
+def test_quantize_pack_sign_modes(flags, kmode, vmode):
+    g = synth.rng(8)
+    cache = oracle.Cache(1, 1, 64)
+    cs = oracle.rope_table(16)
+    k = g.standard_normal((1, 1, 4, 1, 64)).astype(np.float32)
+    v = g.standard_normal((1, 1, 4, 1, 64)).astype(np.float32)
+    pi = synth.rotations(g, 1, 1)
+    S = synth.qjl_matrix(g)
+    lut = LUT32[None, None]
+    oracle.quantize_pack(cache, flags, cs, k, v, [0], [0], pi, lut, lut, S)
+    for j in range(4):
+        kh = oracle.rotated_input(k[0, 0, j, 0], True, j, cs, pi[0, 0])
+        vh = oracle.rotated_input(v[0, 0, j, 0], False, j, cs, pi[0, 0],
+                                  rotate_v=bool(flags & oracle.V_ROTATE))
+        np.testing.assert_array_equal(oracle.unpack_slot(cache.region("k", 0, 0), j),
+                                      oracle.quantize_vector(kh, LUT32, S, kmode)[0])
+        np.testing.assert_array_equal(oracle.unpack_slot(cache.region("v", 0, 0), j),
+                                      oracle.quantize_vector(vh, LUT32, S, vmode)[0])
