@@ -96,7 +96,7 @@ typedef struct tq_params {
   uint32_t flags;          /* TQ_* flags above                                */
   float softmax_scale;     /* logit = score * softmax_scale; <= 0 means 1/8   */
   const float* rope_cs;    /* device [rope_positions][32][2] (cos, sin) from
-                              tq_rope_table; 8-byte aligned                  */
+                              tq_rope_table; 16-byte aligned                 */
   int32_t rope_positions;  /* rows of rope_cs; positions must be below it     */
 } tq_params;
 
@@ -117,7 +117,7 @@ int64_t tq_cache_bytes(int32_t num_layers, int32_t num_heads, int64_t slots);
 /* RoPE cos/sin table (Eq. 2). For position p < positions and pair m < 32:
  *   theta_m = base^(-2m/64),  a = p * theta_m  (both in double precision),
  *   cs[(p*32 + m)*2 + 0] = (float)cos(a),  cs[(p*32 + m)*2 + 1] = (float)sin(a).
- * cs: device, positions*64 floats, 8-byte aligned. base > 0 (10000 for ESM-2). */
+ * cs: device, positions*64 floats, 16-byte aligned. base > 0 (10000 for ESM-2). */
 tq_status tq_rope_table(float* cs, int32_t positions, double base, void* stream);
 
 /* Prefill-side quantizer (Sec. 3.1 prefill steps 1, 3, 4; Sec. 3.3; Sec. 3.4;

@@ -1,0 +1,195 @@
+// C ABI of libturboesm: host-side validation and kernel launches. Every
+// entry point validates its arguments before launching anything, returns a
+// negative tq_status on failure and records a thread-local message.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "../../include/turboesm.h"
+#include "tq_internal.hpp"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+tq_status fail(tq_status code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+tq_status ok() {
+  g_err[0] = '\0';
+  return TQ_OK;
+}
+
+bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+
+tq_status hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(TQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+tq_status check_params(const tq_params* p, bool need_rope) {
+  if (!p) return fail(TQ_ERR_ARG, "params is NULL");
+  if (p->head_dim != 64) return fail(TQ_ERR_DIM, "head_dim must be 64 (got %d)", p->head_dim);
+  if (p->num_layers <= 0 || p->num_heads <= 0)
+    return fail(TQ_ERR_ARG, "num_layers and num_heads must be positive");
+  if (p->io_dtype != TQ_F16 && p->io_dtype != TQ_F32)
+    return fail(TQ_ERR_ARG, "io_dtype must be TQ_F16 or TQ_F32");
+  if (p->flags & ~TQ_FLAGS_ALL) return fail(TQ_ERR_ARG, "unknown flag bits 0x%x", p->flags & ~TQ_FLAGS_ALL);
+  if (need_rope) {
+    if (!p->rope_cs) return fail(TQ_ERR_ARG, "rope_cs is NULL");
+    if (!aligned(p->rope_cs, 16)) return fail(TQ_ERR_ALIGN, "rope_cs must be 16-byte aligned");
+    if (p->rope_positions <= 0) return fail(TQ_ERR_ARG, "rope_positions must be positive");
+  }
+  return ok();
+}
+
+tq_status check_cache(const tq_cache* c) {
+  if (!c) return fail(TQ_ERR_ARG, "cache is NULL");
+  if (!c->k_codes || !c->v_codes || !c->scalars) return fail(TQ_ERR_ARG, "cache buffer is NULL");
+  if (!aligned(c->k_codes, 16) || !aligned(c->v_codes, 16))
+    return fail(TQ_ERR_ALIGN, "cache code planes must be 16-byte aligned");
+  if (!aligned(c->scalars, 8)) return fail(TQ_ERR_ALIGN, "cache scalars must be 8-byte aligned");
+  if (c->slots <= 0 || c->slots % 64 != 0)
+    return fail(TQ_ERR_CAPACITY, "slots must be a positive multiple of 64 (got %lld)", (long long)c->slots);
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tq_last_error(void) { return g_err; }
+
+const char* tq_version(void) { return "turboesm-gfx950 0.1.0"; }
+
+int64_t tq_cache_bytes(int32_t num_layers, int32_t num_heads, int64_t slots) {
+  if (num_layers < 0 || num_heads < 0 || slots < 0) return -1;
+  return (int64_t)num_layers * num_heads * slots * 72;
+}
+
+tq_status tq_rope_table(float* cs, int32_t positions, double base, void* stream) {
+  if (!cs) return fail(TQ_ERR_ARG, "cs is NULL");
+  if (!aligned(cs, 16)) return fail(TQ_ERR_ALIGN, "cs must be 16-byte aligned");
+  if (positions <= 0) return fail(TQ_ERR_ARG, "positions must be positive");
+  if (!(base > 0.0) || !std::isfinite(base)) return fail(TQ_ERR_ARG, "base must be positive and finite");
+  return hip_status(tq::launch_rope_table(cs, positions, base, (hipStream_t)stream), "tq_rope_table launch");
+}
+
+tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache, const void* k,
+                           const void* v, int32_t B, int32_t T, int32_t layer0, int32_t nlayers,
+                           const int32_t* pos0, const int64_t* slot0, const float* pi,
+                           const float* lut_k, const float* lut_v, const float* qjl_s,
+                           const float* ebar, void* stream) {
+  (void)ebar;
+  const bool rotated = params && (params->flags & TQ_INPUT_ROTATED);
+  tq_status s = check_params(params, !rotated);
+  if (s != TQ_OK) return s;
+  if ((s = check_cache(cache)) != TQ_OK) return s;
+  if (B < 0 || T < 0 || nlayers < 0) return fail(TQ_ERR_ARG, "B, T and nlayers must be >= 0");
+  if (layer0 < 0 || layer0 + nlayers > params->num_layers)
+    return fail(TQ_ERR_DIM, "layers [%d, %d) outside [0, %d)", layer0, layer0 + nlayers, params->num_layers);
+  if ((int64_t)B * T * nlayers == 0) return ok();
+  if (!k || !v || !pos0 || !slot0 || !pi || !lut_k || !lut_v || !qjl_s)
+    return fail(TQ_ERR_ARG, "a required pointer is NULL");
+  if (!aligned(k, 16) || !aligned(v, 16)) return fail(TQ_ERR_ALIGN, "k and v must be 16-byte aligned");
+  if (!aligned(pi, 16) || !aligned(qjl_s, 16)) return fail(TQ_ERR_ALIGN, "pi and qjl_s must be 16-byte aligned");
+  if ((int64_t)nlayers * B * T * params->num_heads >= ((int64_t)1 << 40))
+    return fail(TQ_ERR_ARG, "too many token-heads");
+  if ((int64_t)B * params->num_heads > 65535 || nlayers > 65535)
+    return fail(TQ_ERR_ARG, "B*H and nlayers must be <= 65535");
+  tq::QuantArgs a{};
+  a.k = k; a.v = v;
+  a.B = B; a.T = T; a.H = params->num_heads; a.layer0 = layer0; a.nlayers = nlayers;
+  a.f16 = params->io_dtype == TQ_F16;
+  a.flags = params->flags;
+  a.rope_cs = params->rope_cs; a.rope_positions = params->rope_positions;
+  a.pos0 = pos0; a.slot0 = slot0; a.pi = pi; a.lut_k = lut_k; a.lut_v = lut_v; a.qjl_s = qjl_s;
+  a.k_codes = (uint8_t*)cache->k_codes; a.v_codes = (uint8_t*)cache->v_codes;
+  a.scalars = (uint16_t*)cache->scalars; a.slots = cache->slots;
+  return hip_status(tq::launch_quantize(a, (hipStream_t)stream), "tq_quantize_pack launch");
+}
+
+size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B, int32_t nlayers, int32_t max_len) {
+  if (!params || params->num_heads <= 0 || B <= 0 || nlayers <= 0 || max_len < 0) return 0;
+  const int64_t units = (int64_t)nlayers * B * params->num_heads;
+  int nsplit, split_tiles;
+  tq::decode_plan((int)std::min<int64_t>(units, 1 << 30), max_len, &nsplit, &split_tiles);
+  if (nsplit <= 1) return 0;
+  const size_t part = (size_t)units * nsplit * tq::kPartialFloats * sizeof(float);
+  const size_t cnt = (size_t)units * sizeof(uint32_t);
+  return ((part + 255) / 256) * 256 + cnt;
+}
+
+tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const void* q, int32_t B,
+                           int32_t layer0, int32_t nlayers, const int32_t* q_pos,
+                           const int64_t* seq_slot0, const int32_t* seq_len, int32_t max_len,
+                           const float* pi, const float* lut_k, const float* lut_v,
+                           const float* qjl_s, const float* ebar, void* out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  tq_status s = check_params(params, true);
+  if (s != TQ_OK) return s;
+  if ((s = check_cache(cache)) != TQ_OK) return s;
+  if (params->flags & TQ_INPUT_ROTATED) return fail(TQ_ERR_ARG, "TQ_INPUT_ROTATED applies to tq_quantize_pack only");
+  if (B < 0 || nlayers < 0 || max_len < 0) return fail(TQ_ERR_ARG, "B, nlayers and max_len must be >= 0");
+  if (layer0 < 0 || layer0 + nlayers > params->num_layers)
+    return fail(TQ_ERR_DIM, "layers [%d, %d) outside [0, %d)", layer0, layer0 + nlayers, params->num_layers);
+  if ((int64_t)B * nlayers == 0) return ok();
+  if (!q || !q_pos || !seq_slot0 || !seq_len || !pi || !lut_k || !lut_v || !qjl_s || !out)
+    return fail(TQ_ERR_ARG, "a required pointer is NULL");
+  if ((params->flags & TQ_QJL_PAPER) && !ebar) return fail(TQ_ERR_ARG, "TQ_QJL_PAPER needs ebar");
+  if (!aligned(q, 16) || !aligned(out, 16)) return fail(TQ_ERR_ALIGN, "q and out must be 16-byte aligned");
+  if (!aligned(pi, 16) || !aligned(qjl_s, 16)) return fail(TQ_ERR_ALIGN, "pi and qjl_s must be 16-byte aligned");
+  if ((int64_t)max_len > cache->slots) return fail(TQ_ERR_CAPACITY, "max_len exceeds the cache slots");
+  const int64_t units = (int64_t)nlayers * B * params->num_heads;
+  if (units >= ((int64_t)1 << 31)) return fail(TQ_ERR_ARG, "too many (layer, sequence, head) units");
+  int nsplit, split_tiles;
+  tq::decode_plan((int)units, max_len, &nsplit, &split_tiles);
+  const size_t need = tq_decode_workspace_bytes(params, B, nlayers, max_len);
+  if (need > 0) {
+    if (!workspace) return fail(TQ_ERR_CAPACITY, "workspace of %zu bytes required", need);
+    if (workspace_bytes < need)
+      return fail(TQ_ERR_CAPACITY, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+    if (!aligned(workspace, 16)) return fail(TQ_ERR_ALIGN, "workspace must be 16-byte aligned");
+  }
+  if (units * nsplit > ((int64_t)1 << 31) - 8) return fail(TQ_ERR_ARG, "grid too large");
+  const float scale = params->softmax_scale > 0.0f ? params->softmax_scale : 0.125f;
+  tq::DecodeArgs a{};
+  a.q = q; a.B = B; a.H = params->num_heads; a.layer0 = layer0; a.nlayers = nlayers;
+  a.f16_in = params->io_dtype == TQ_F16;
+  a.f16_out = (params->io_dtype == TQ_F16) && !(params->flags & TQ_OUT_FP32);
+  a.flags = params->flags;
+  a.logit_scale2 = (float)((double)scale * 1.4426950408889634 / 8.0);
+  a.rope_cs = params->rope_cs; a.rope_positions = params->rope_positions;
+  a.q_pos = q_pos; a.seq_slot0 = seq_slot0; a.seq_len = seq_len; a.max_len = max_len;
+  a.pi = pi; a.lut_k = lut_k; a.lut_v = lut_v; a.qjl_s = qjl_s; a.ebar = ebar;
+  a.k_codes = (const uint8_t*)cache->k_codes; a.v_codes = (const uint8_t*)cache->v_codes;
+  a.scalars = (const uint16_t*)cache->scalars; a.slots = cache->slots;
+  a.out = out;
+  a.nsplit = nsplit; a.split_tiles = split_tiles;
+  if (need > 0) {
+    const size_t part = (size_t)units * nsplit * tq::kPartialFloats * sizeof(float);
+    a.partials = (float*)workspace;
+    a.counters = (uint32_t*)((char*)workspace + ((part + 255) / 256) * 256);
+  }
+  return hip_status(tq::launch_decode(a, (hipStream_t)stream), "tq_decode_attend launch");
+}
+
+tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal, float* pi_out,
+                                float* sing_out, void* stream) {
+  if (nheads < 0 || ncal < 0) return fail(TQ_ERR_ARG, "nheads and ncal must be >= 0");
+  if (nheads == 0) return ok();
+  if (!x || !pi_out) return fail(TQ_ERR_ARG, "x and pi_out must not be NULL");
+  if (ncal == 0) return fail(TQ_ERR_ARG, "ncal must be positive");
+  if (nheads > 65535 * 1024) return fail(TQ_ERR_ARG, "too many heads");
+  return hip_status(tq::launch_calibrate(x, nheads, ncal, pi_out, sing_out, (hipStream_t)stream),
+                    "tq_calibrate_rotation launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,168 @@
+// Head-wise rotation calibration (TurboESM Sec. 3.2): for the post-RoPE keys
+// X (ncal x 64) of one head, Pi = V^T where X = U Sigma V^T.
+//
+// One block per head. The Gram matrix G = X^T X is accumulated in fp64 and
+// diagonalized in LDS by cyclic Jacobi rotations in the round-robin
+// (tournament) order: each of the 63 rounds of a sweep applies 32 disjoint
+// plane rotations at once. Eigenvalues of G are sigma^2; eigenvectors are the
+// right singular vectors. Rows of Pi are ordered by descending sigma and
+// signed so that each row's largest-magnitude entry is positive (lowest
+// index on ties).
+#include "tq_device.hpp"
+#include "tq_internal.hpp"
+
+namespace tq {
+
+constexpr int kMaxSweeps = 40;
+constexpr int kStageRows = 32;
+
+struct CalibSmem {
+  double G[kDim * kDim];
+  double V[kDim * kDim];
+  float xs[kStageRows * kDim];
+  double c[kPairs], s[kPairs];
+  int p[kPairs], q[kPairs];
+  double red[256];
+  int rank[kDim];
+  int done;
+};
+
+__device__ __forceinline__ int tournament_player(int pos, int round) {
+  return pos == 0 ? 0 : ((pos - 1 + round) % (kDim - 1)) + 1;
+}
+
+__global__ __launch_bounds__(256) void calibrate_kernel(const float* x, int ncal, float* pi_out,
+                                                        float* sing_out) {
+  __shared__ CalibSmem sm;
+  const int head = blockIdx.x;
+  const int t = threadIdx.x;
+  const float* X = x + (int64_t)head * ncal * kDim;
+
+  // ---- Gram matrix in fp64: thread t owns entries e = t + 256 r
+  double acc[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.0;
+  for (int row0 = 0; row0 < ncal; row0 += kStageRows) {
+    const int rows = min(kStageRows, ncal - row0);
+    for (int e = t; e < kStageRows * kDim; e += 256)
+      sm.xs[e] = (e / kDim < rows) ? X[(int64_t)row0 * kDim + e] : 0.0f;
+    __syncthreads();
+    for (int rr = 0; rr < rows; ++rr) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int e = t + 256 * r;
+        acc[r] = fma((double)sm.xs[rr * kDim + (e >> 6)], (double)sm.xs[rr * kDim + (e & 63)], acc[r]);
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int e = t + 256 * r;
+    sm.G[e] = acc[r];
+    sm.V[e] = ((e >> 6) == (e & 63)) ? 1.0 : 0.0;
+  }
+  __syncthreads();
+
+  // ---- cyclic Jacobi, round-robin order
+  for (int sweep = 0; sweep < kMaxSweeps; ++sweep) {
+    // convergence: off-diagonal mass versus diagonal mass
+    double off = 0.0, dia = 0.0;
+    for (int e = t; e < kDim * kDim; e += 256) {
+      const double g = sm.G[e];
+      if ((e >> 6) == (e & 63)) dia += g * g; else off += g * g;
+    }
+    sm.red[t] = off;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if (t < w) sm.red[t] += sm.red[t + w];
+      __syncthreads();
+    }
+    const double off_tot = sm.red[0];
+    __syncthreads();
+    sm.red[t] = dia;
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if (t < w) sm.red[t] += sm.red[t + w];
+      __syncthreads();
+    }
+    const double dia_tot = sm.red[0];
+    __syncthreads();
+    if (off_tot <= 1e-30 * dia_tot || off_tot == 0.0) break;
+
+    for (int round = 0; round < kDim - 1; ++round) {
+      if (t < kPairs) {
+        int a = tournament_player(t, round), b = tournament_player(kDim - 1 - t, round);
+        if (a > b) { const int tmp = a; a = b; b = tmp; }
+        const double gpq = sm.G[a * kDim + b];
+        double c = 1.0, s = 0.0;
+        if (gpq != 0.0) {
+          const double tau = (sm.G[b * kDim + b] - sm.G[a * kDim + a]) / (2.0 * gpq);
+          double tn;
+          if (fabs(tau) > 1e150) {
+            tn = 0.5 / tau;
+          } else {
+            tn = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+          }
+          c = 1.0 / sqrt(1.0 + tn * tn);
+          s = tn * c;
+        }
+        sm.p[t] = a; sm.q[t] = b; sm.c[t] = c; sm.s[t] = s;
+      }
+      __syncthreads();
+      // G <- G J (columns p, q)
+      for (int e = t; e < kPairs * kDim; e += 256) {
+        const int k = e >> 6, r = e & 63;
+        const int a = sm.p[k], b = sm.q[k];
+        const double c = sm.c[k], s = sm.s[k];
+        const double ga = sm.G[r * kDim + a], gb = sm.G[r * kDim + b];
+        sm.G[r * kDim + a] = c * ga - s * gb;
+        sm.G[r * kDim + b] = s * ga + c * gb;
+      }
+      __syncthreads();
+      // G <- J^T G (rows p, q) and V <- V J (columns p, q)
+      for (int e = t; e < kPairs * kDim; e += 256) {
+        const int k = e >> 6, r = e & 63;
+        const int a = sm.p[k], b = sm.q[k];
+        const double c = sm.c[k], s = sm.s[k];
+        const double ga = sm.G[a * kDim + r], gb = sm.G[b * kDim + r];
+        sm.G[a * kDim + r] = c * ga - s * gb;
+        sm.G[b * kDim + r] = s * ga + c * gb;
+        const double va = sm.V[r * kDim + a], vb = sm.V[r * kDim + b];
+        sm.V[r * kDim + a] = c * va - s * vb;
+        sm.V[r * kDim + b] = s * va + c * vb;
+      }
+      __syncthreads();
+    }
+  }
+
+  // ---- order by descending eigenvalue, canonical signs, write Pi and sigma
+  if (t < kDim) {
+    const double lt = sm.G[t * kDim + t];
+    int rank = 0;
+    for (int b = 0; b < kDim; ++b) {
+      const double lb = sm.G[b * kDim + b];
+      rank += (lb > lt || (lb == lt && b < t)) ? 1 : 0;
+    }
+    sm.rank[t] = rank;
+    // column t of V is the eigenvector of eigenvalue lt
+    int arg = 0;
+    double best = -1.0;
+    for (int k = 0; k < kDim; ++k) {
+      const double v = fabs(sm.V[k * kDim + t]);
+      if (v > best) { best = v; arg = k; }
+    }
+    const double sg = (sm.V[arg * kDim + t] < 0.0) ? -1.0 : 1.0;
+    float* dst = pi_out + ((int64_t)head * kDim + rank) * kDim;
+    for (int k = 0; k < kDim; ++k) dst[k] = (float)(sg * sm.V[k * kDim + t]);
+    if (sing_out) sing_out[(int64_t)head * kDim + rank] = (float)sqrt(lt > 0.0 ? lt : 0.0);
+  }
+}
+
+hipError_t launch_calibrate(const float* x, int nheads, int ncal, float* pi_out, float* sing_out,
+                            hipStream_t st) {
+  hipLaunchKernelGGL(calibrate_kernel, dim3(nheads), dim3(256), 0, st, x, ncal, pi_out, sing_out);
+  return hipGetLastError();
+}
+
+}  // namespace tq

@@ -1,0 +1,140 @@
+// Device-side building blocks shared by the quantize and decode kernels.
+//
+// Cache layout (64-slot tiles, 2048 bytes per tile per tensor):
+//   K tile, token-major: 16-byte half c (codes 32c..32c+31) of slot-in-tile r
+//        at byte (c*64 + r)*16. One lane per token loads its 32 bytes with two
+//        128-bit loads; each wave-wide load covers 1 KiB contiguously.
+//   V tile, dimension-major: 16-byte half c (slots 32c..32c+31) of dimension i
+//        at byte (c*64 + i)*16. One lane per dimension loads the 64 codes of its
+//        dimension for the whole tile with two 128-bit loads.
+//   A nibble is idx | sign << 3; nibble j of a 32-bit word sits at bits 4j..4j+3.
+//   Scalars: 4 x fp16 per slot [n_k, g_k, n_v, g_v] at byte slot*8.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_fp16.h>
+#include <stdint.h>
+
+namespace tq {
+
+constexpr int kDim = 64;
+constexpr int kTile = 64;
+constexpr int kTileBytes = 2048;   // 64 slots x 32 bytes
+constexpr int kPairs = 32;
+
+// Flags (values fixed by the public header).
+constexpr uint32_t kVRotate = 1u << 0;
+constexpr uint32_t kVQjl = 1u << 1;
+constexpr uint32_t kQjlPaper = 1u << 2;
+constexpr uint32_t kRopeHalf = 1u << 3;
+constexpr uint32_t kInputRotated = 1u << 4;
+constexpr uint32_t kOutF32 = 1u << 5;
+
+// sqrt(pi/2) / m with m = 64 projection rows (QJL estimator scale).
+constexpr float kQjlAlpha = 0.019583033395554691f;
+
+__device__ __forceinline__ float load_in(const void* p, int64_t i, bool f16) {
+  if (f16) return __half2float(reinterpret_cast<const __half*>(p)[i]);
+  return reinterpret_cast<const float*>(p)[i];
+}
+
+// Norms are stored as fp16 with round-to-nearest-even, saturated at 65504.
+__device__ __forceinline__ uint32_t store_norm(float x) {
+  x = (x > 65504.0f) ? 65504.0f : x;
+  return (uint32_t)__half_as_ushort(__float2half_rn(x));
+}
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t bits) {
+  return __half2float(__ushort_as_half((unsigned short)(bits & 0xFFFFu)));
+}
+
+// Byte offset of 16-byte half c of row r (slot for K, dimension for V) in a tile.
+__device__ __forceinline__ int64_t tile_half_offset(int64_t tile, int c, int r) {
+  return tile * kTileBytes + (int64_t)(c * kTile + r) * 16;
+}
+
+// Fixed-order binary32 steps of the quantizer for one vector held in registers
+// (this file is compiled with -ffp-contract=off and correctly rounded sqrtf and
+// division, the HIP defaults; fmaf is the only fused operation)
+// by one lane: the norm and residual-norm fma chains run over i ascending and
+// the projected sign of row i is an fma chain over k ascending, so any kernel
+// that calls this on the same x^ produces the same bits.
+//   xh[64]   rotated vector (overwritten by the residual r)
+//   c[8]     ascending table, t[7] its midpoints (0.5f * (c_m + c_{m+1}))
+//   S        64 x 64 projection in LDS (row-major); unused unless sign_mode == 1
+//   sign_mode 0 none, 1 projected (S r), 2 per element (r)
+//   words[8] out: nibble words (idx | sign << 3)
+struct QuantOut {
+  uint32_t n16, g16;
+};
+
+__device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const float (&c)[8],
+                                                  const float (&t)[7], const float* S,
+                                                  int sign_mode, uint32_t (&words)[8]) {
+  float s = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kDim; ++i) s = fmaf(xh[i], xh[i], s);
+  const float n = sqrtf(s);
+  const float inv = (n == 0.0f) ? 0.0f : 8.0f / n;
+#pragma unroll
+  for (int w = 0; w < 8; ++w) words[w] = 0u;
+#pragma unroll
+  for (int i = 0; i < kDim; ++i) {
+    const float u = xh[i] * inv;
+    uint32_t idx = 0;
+    float lv = c[0];
+#pragma unroll
+    for (int m = 0; m < 7; ++m) {
+      const bool above = u > t[m];
+      idx += above ? 1u : 0u;
+      lv = above ? c[m + 1] : lv;
+    }
+    words[i >> 3] |= idx << (4 * (i & 7));
+    xh[i] = u - lv;   // residual r_i
+  }
+  float gs = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kDim; ++i) gs = fmaf(xh[i], xh[i], gs);
+  const float g = sqrtf(gs);
+  uint64_t sbits = 0;
+  if (sign_mode == 1) {
+    for (int i = 0; i < kDim; ++i) {
+      float acc = 0.0f;
+      const float4* row = reinterpret_cast<const float4*>(S + i * kDim);
+#pragma unroll
+      for (int k4 = 0; k4 < kDim / 4; ++k4) {
+        const float4 sv = row[k4];
+        acc = fmaf(sv.x, xh[4 * k4 + 0], acc);
+        acc = fmaf(sv.y, xh[4 * k4 + 1], acc);
+        acc = fmaf(sv.z, xh[4 * k4 + 2], acc);
+        acc = fmaf(sv.w, xh[4 * k4 + 3], acc);
+      }
+      sbits |= (uint64_t)((acc < 0.0f) ? 0u : 1u) << i;
+    }
+  } else if (sign_mode == 2) {
+#pragma unroll
+    for (int i = 0; i < kDim; ++i) sbits |= (uint64_t)((xh[i] < 0.0f) ? 0u : 1u) << i;
+  }
+#pragma unroll
+  for (int i = 0; i < kDim; ++i)
+    words[i >> 3] |= (uint32_t)((sbits >> i) & 1u) << (4 * (i & 7) + 3);
+  QuantOut o;
+  o.n16 = store_norm(n);
+  o.g16 = (sign_mode == 0) ? 0u : store_norm(g);
+  return o;
+}
+
+// Wave-wide reductions (64 lanes).
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace tq

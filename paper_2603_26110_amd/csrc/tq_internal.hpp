@@ -1,0 +1,70 @@
+// Host/device argument blocks and launchers shared by the C-ABI translation
+// unit and the kernel translation units. Not part of the public interface.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tq {
+
+struct QuantArgs {
+  const void* k;
+  const void* v;
+  int B, T, H, layer0, nlayers;
+  int f16;                 // k, v are fp16 (else fp32)
+  uint32_t flags;
+  const float* rope_cs;
+  int rope_positions;
+  const int32_t* pos0;
+  const int64_t* slot0;
+  const float* pi;
+  const float* lut_k;
+  const float* lut_v;
+  const float* qjl_s;
+  uint8_t* k_codes;
+  uint8_t* v_codes;
+  uint16_t* scalars;
+  int64_t slots;
+};
+
+struct DecodeArgs {
+  const void* q;
+  int B, H, layer0, nlayers;
+  int f16_in;              // q is fp16
+  int f16_out;             // out is fp16
+  uint32_t flags;
+  float logit_scale2;      // softmax_scale * log2(e) / 8 (applied to n_k * (A + coef B))
+  const float* rope_cs;
+  int rope_positions;
+  const int32_t* q_pos;
+  const int64_t* seq_slot0;
+  const int32_t* seq_len;
+  int max_len;
+  const float* pi;
+  const float* lut_k;
+  const float* lut_v;
+  const float* qjl_s;
+  const float* ebar;
+  const uint8_t* k_codes;
+  const uint8_t* v_codes;
+  const uint16_t* scalars;
+  int64_t slots;
+  void* out;
+  float* partials;         // [units][nsplit][kPartialFloats]
+  uint32_t* counters;      // [units]
+  int nsplit;              // splits per unit
+  int split_tiles;         // 64-token tiles per split
+};
+
+constexpr int kPartialFloats = 2 * 64 + 4;   // m, l, pad, pad, o[64], s[64]
+
+// Launchers (return the HIP status of the launch).
+hipError_t launch_rope_table(float* cs, int positions, double base, hipStream_t st);
+hipError_t launch_quantize(const QuantArgs& a, hipStream_t st);
+void decode_plan(int units, int max_len, int* nsplit, int* split_tiles);
+hipError_t launch_decode(const DecodeArgs& a, hipStream_t st);
+hipError_t launch_calibrate(const float* x, int nheads, int ncal, float* pi_out,
+                            float* sing_out, hipStream_t st);
+
+}  // namespace tq

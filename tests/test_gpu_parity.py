@@ -1,0 +1,282 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Quantizer: bit-exact codes and fp16 scalars given identical rotated inputs
+(TQ_INPUT_ROTATED), on both quantize kernels (T >= 64 one lane per token,
+T < 64 one wave per vector), ragged and unaligned slots, every sign mode.
+End to end (raw keys/values, GPU RoPE and rotation in binary32): codes may
+differ only where the oracle's fp64 coordinate sits within rounding of a
+decision threshold.
+Decode: GPU output against the fp64 oracle run on the very cache bytes the
+GPU wrote, |err| <= 2e-3 (fp32 output), fp16 output within max(2e-3, 1 ulp).
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2603_26110_amd as tq
+from gpu_cases import Case, GAUSS_LUT, fp16_ulp, to_oracle
+from oracle import oracle
+from paper_2603_26110_amd import synth
+
+pytestmark = pytest.mark.gpu
+TOL = 2e-3
+
+
+def test_library_loaded_and_version():
+    assert tq.version().startswith("turboesm-gfx950")
+    import os
+    maps = open(f"/proc/{os.getpid()}/maps").read()
+    assert tq.lib_path in maps
+
+
+def test_rope_table_matches_oracle():
+    cs = tq.rope_table(8256).cpu().numpy()
+    ref = oracle.rope_table(8256)
+    diff = np.abs(cs.astype(np.float64) - ref)
+    ulp = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64)
+    assert np.all(diff <= ulp)
+    assert np.mean(cs == ref) > 0.999
+
+
+# ------------------------------------------------------------------ quantizer
+def _rotated_inputs(seed, L, B, T, H):
+    g = synth.rng(seed)
+    scale = g.uniform(0.05, 40.0, (L, B, T, H, 1)).astype(np.float32)
+    kh = (g.standard_normal((L, B, T, H, 64)) * scale).astype(np.float32)
+    vh = (g.standard_t(4, (L, B, T, H, 64)) * scale).astype(np.float32)
+    # special vectors: zero, constant, huge norm, coordinates on a threshold
+    kh[0, 0, 0, 0] = 0.0
+    kh[0, 0, min(1, T - 1), 0] = 0.75
+    vh[0, 0, min(2, T - 1), 0] = 30000.0
+    return kh, vh
+
+
+@pytest.mark.parametrize("T,B,slot0,flags", [
+    (256, 1, [0], tq.V_ROTATE),                       # whole tiles, tile kernel
+    (200, 2, [64, 640], tq.V_ROTATE),                 # ragged tail
+    (130, 2, [37, 300], tq.V_ROTATE),                 # unaligned slots
+    (96, 1, [5], tq.V_QJL | tq.V_ROTATE),             # V sign bits
+    (70, 1, [0], tq.QJL_PAPER),                       # per-element signs
+    (70, 1, [3], tq.QJL_PAPER | tq.V_QJL),
+    (1, 3, [0, 100, 1027], tq.V_ROTATE),              # appends: wave kernel
+    (5, 2, [61, 200], tq.V_QJL | tq.V_ROTATE),
+    (33, 1, [7], tq.QJL_PAPER | tq.V_QJL),
+])
+def test_quantize_bit_exact_on_rotated_inputs(T, B, slot0, flags):
+    L, H = 2, 3
+    flags |= tq.INPUT_ROTATED
+    case = Case(11, L, H, B, T, io="f32", flags=flags, slots=1152, slot0=slot0, layer0=1, nl=1)
+    kh, vh = _rotated_inputs(T * 7 + B, 1, B, T, H)
+    cache = tq.Cache(L, H, 1152)
+    case.gpu_quantize(cache, k=torch.from_numpy(kh).cuda(), v=torch.from_numpy(vh).cuda())
+    torch.cuda.synchronize()
+    oc = oracle.Cache(L, H, 1152)
+    case.oracle_quantize(oc, k=kh, v=vh)
+    got = to_oracle(cache)
+    np.testing.assert_array_equal(got.s, oc.s)
+    np.testing.assert_array_equal(got.k, oc.k)
+    np.testing.assert_array_equal(got.v, oc.v)
+    assert oc.s.any()
+
+
+def test_quantize_kernels_agree_on_raw_inputs():
+    # The tile kernel (T >= 64) and the wave kernel (T < 64) rotate in the
+    # same fma order, so they must write identical bytes for the same tokens.
+    L, H, T = 1, 4, 64
+    case = Case(12, L, H, 1, T, io="f16", slots=128)
+    a = tq.Cache(L, H, 128)
+    case.gpu_quantize(a)
+    b = tq.Cache(L, H, 128)
+    for j0 in range(0, T, 16):
+        sl = slice(j0, j0 + 16)
+        case.gpu_quantize(b, k=case.t("k")[:, :, sl].contiguous(), v=case.t("v")[:, :, sl].contiguous(),
+                          pos0=[j0], slot0=[j0])
+    torch.cuda.synchronize()
+    assert torch.equal(a.k_codes, b.k_codes)
+    assert torch.equal(a.v_codes, b.v_codes)
+    assert torch.equal(a.scalars, b.scalars)
+
+
+def _threshold_distance(case, oc_flags, li, b, j, h, is_key):
+    x = (case.k if is_key else case.v)[li, b, j, h].astype(np.float32)
+    l = case.layer0 + li
+    xh = oracle.rotated_input(x, is_key, int(case.pos0[b]) + j, case.cs_host, case.pi[l, h],
+                              rotate_v=bool(oc_flags & tq.V_ROTATE))
+    xd = xh.astype(np.float64)
+    u = xd * 8.0 / np.linalg.norm(xd)
+    lut = (case.lut_k if is_key else case.lut_v)[l, h].astype(np.float64)
+    t = 0.5 * (lut[:-1] + lut[1:])
+    return np.min(np.abs(u[:, None] - t[None, :]), axis=1)
+
+
+@pytest.mark.parametrize("T", [256, 3])
+def test_quantize_end_to_end_matches_up_to_threshold_rounding(T):
+    L, H, B = 1, 8, 2
+    case = Case(13, L, H, B, T, io="f16", slots=2 * 320, slot0=[0, 320], pos0=[0, 17])
+    cache = tq.Cache(L, H, case.slots)
+    case.gpu_quantize(cache)
+    torch.cuda.synchronize()
+    oc = oracle.Cache(L, H, case.slots)
+    case.oracle_quantize(oc)
+    got = to_oracle(cache)
+    # norms: fp16 of binary32 norms of vectors that agree to ~1e-6
+    ng = got.s.view(np.float16).astype(np.float64)
+    no = oc.s.view(np.float16).astype(np.float64)
+    assert np.all(np.abs(ng - no) <= fp16_ulp(no) + 1e-12)
+    code_diff = 0
+    sign_diff = 0
+    total = 0
+    for b in range(B):
+        for j in range(T):
+            s = int(case.slot0[b]) + j
+            for h in range(H):
+                for is_key, which in ((True, "k"), (False, "v")):
+                    ng_ = oracle.unpack_slot(got.region(which, 0, h), s)
+                    no_ = oracle.unpack_slot(oc.region(which, 0, h), s)
+                    total += 64
+                    bad = (ng_ & 7) != (no_ & 7)
+                    sign_diff += int(((ng_ >> 3) != (no_ >> 3)).sum())
+                    if bad.any():
+                        code_diff += int(bad.sum())
+                        dist = _threshold_distance(case, case.flags, 0, b, j, h, is_key)
+                        assert np.all(dist[bad] < 1e-4), (b, j, h, which, dist[bad])
+                        assert np.all(np.abs((ng_[bad] & 7).astype(int) - (no_[bad] & 7)) == 1)
+    assert code_diff <= 1e-3 * total
+    assert sign_diff <= 64 * code_diff + 1e-4 * total
+
+
+# --------------------------------------------------------------------- decode
+def _decode_check(case, cache, q_pos, seq_slot0, seq_len, max_len, flags=None):
+    flags = case.flags if flags is None else flags
+    out32 = case.gpu_decode(cache, q_pos, seq_slot0, seq_len, max_len, flags=flags | tq.OUT_FP32)
+    torch.cuda.synchronize()
+    ref = case.oracle_decode(to_oracle(cache), q_pos, seq_slot0, seq_len, flags=flags)
+    got = out32.cpu().numpy().astype(np.float64)
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got) == np.isfinite(ref))
+    fin = np.isfinite(ref)
+    assert np.max(err[fin], initial=0.0) <= TOL, np.max(err[fin])
+    if case.io == "f16":
+        out16 = case.gpu_decode(cache, q_pos, seq_slot0, seq_len, max_len, flags=flags)
+        torch.cuda.synchronize()
+        g16 = out16.cpu().numpy().astype(np.float64)
+        r16 = ref.astype(np.float16).astype(np.float64)
+        lim = np.maximum(TOL, fp16_ulp(r16))
+        assert np.all(np.abs(g16 - r16)[fin] <= lim[fin])
+    return got, ref
+
+
+def test_decode_tiny_fp32_workload():
+    # 1 layer, 1 head, 256 cached tokens, fp32 I/O, one query at position 256.
+    case = Case(20260, 1, 1, 1, 256, io="f32", slots=320, slot0=[0])
+    cache = tq.Cache(1, 1, 320)
+    case.gpu_quantize(cache)
+    _decode_check(case, cache, [256], [0], [256], 256)
+
+
+@pytest.mark.parametrize("flags", [tq.V_ROTATE, 0, tq.V_ROTATE | tq.V_QJL, tq.QJL_PAPER,
+                                   tq.QJL_PAPER | tq.V_QJL | tq.V_ROTATE,
+                                   tq.ROPE_HALF | tq.V_ROTATE])
+def test_decode_flags(flags):
+    case = Case(21, 2, 4, 2, 300, io="f16", flags=flags, slots=2 * 384, slot0=[0, 384])
+    cache = tq.Cache(2, 4, case.slots)
+    case.gpu_quantize(cache)
+    _decode_check(case, cache, [300, 310], [0, 384], [300, 257], 320)
+
+
+@pytest.mark.parametrize("lens", [[1], [63], [64], [65], [0], [1024], [1025]])
+def test_decode_lengths(lens):
+    n = max(lens)
+    case = Case(22, 1, 3, len(lens), max(n, 1), io="f16", slots=1088)
+    cache = tq.Cache(1, 3, 1088)
+    case.gpu_quantize(cache)
+    got, ref = _decode_check(case, cache, [n], [0], lens, max(n, 1))
+    if lens[0] == 0:
+        assert np.all(got == 0)
+
+
+def test_decode_ragged_batch_and_split_k():
+    # lengths spread over [1, 1100]; max_len drives the split count
+    g = synth.rng(23)
+    B = 12
+    lens = g.integers(1, 1100, B).astype(np.int32)
+    offs, slots = synth.tile_aligned_offsets(lens)
+    case = Case(23, 1, 5, B, int(lens.max()), io="f16", slots=slots, slot0=offs)
+    cache = tq.Cache(1, 5, slots)
+    # quantize each sequence's own length
+    for b in range(B):
+        sl = slice(0, int(lens[b]))
+        case.gpu_quantize(cache, k=case.t("k")[:, b:b + 1, sl].contiguous(),
+                          v=case.t("v")[:, b:b + 1, sl].contiguous(), pos0=[0], slot0=[int(offs[b])])
+    qpos = lens.copy()
+    _decode_check(case, cache, qpos, offs, lens, int(lens.max()))
+    # a larger max_len bound (more splits) gives the same answer within rounding
+    out_a = case.gpu_decode(cache, qpos, offs, lens, int(lens.max()), flags=case.flags | tq.OUT_FP32)
+    out_b = case.gpu_decode(cache, qpos, offs, lens, int(slots), flags=case.flags | tq.OUT_FP32)
+    torch.cuda.synchronize()
+    assert torch.max(torch.abs(out_a - out_b)).item() < 1e-5
+
+
+def test_decode_invalid_sequences_give_nan():
+    case = Case(24, 1, 2, 3, 64, io="f16", slots=256, slot0=[0, 64, 128])
+    cache = tq.Cache(1, 2, 256)
+    case.gpu_quantize(cache)
+    # misaligned start, query position outside the table, length above max_len
+    out = case.gpu_decode(cache, [64, 10 ** 6, 64], [1, 64, 128], [10, 10, 70], 64,
+                          flags=case.flags | tq.OUT_FP32)
+    o = out.cpu().numpy()
+    assert np.all(np.isnan(o[:, 0])) and np.all(np.isnan(o[:, 1])) and np.all(np.isnan(o[:, 2]))
+
+
+def test_decode_is_deterministic():
+    case = Case(25, 2, 4, 1, 900, io="f16", slots=960)
+    cache = tq.Cache(2, 4, 960)
+    case.gpu_quantize(cache)
+    a = case.gpu_decode(cache, [900], [0], [900], 900)
+    b = case.gpu_decode(cache, [900], [0], [900], 900)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_decode_steps_append_then_attend():
+    # one layer of 20 heads: prefill 1024 tokens, then 8 steps of
+    # (quantize the new token at position len, attend over len + 1 tokens)
+    L, H, T, steps = 1, 20, 1024, 8
+    case = Case(20261, L, H, 1, T + steps, io="f16", slots=1088, slot0=[0])
+    cache = tq.Cache(L, H, 1088)
+    case.gpu_quantize(cache, k=case.t("k")[:, :, :T].contiguous(), v=case.t("v")[:, :, :T].contiguous())
+    for s in range(steps):
+        n = T + s
+        case.gpu_quantize(cache, k=case.t("k")[:, :, n:n + 1].contiguous(),
+                          v=case.t("v")[:, :, n:n + 1].contiguous(), pos0=[n], slot0=[n])
+        _decode_check(case, cache, [n], [0], [n + 1], 1088)
+
+
+# ---------------------------------------------------------------- calibration
+def test_calibrate_rotation_matches_svd():
+    g = synth.rng(30)
+    nh, ncal = 6, 4096
+    cs = oracle.rope_table(1024)
+    ch = synth.outlier_channels(g, 1, nh)
+    keys = synth.keys(g, 1, 1, ncal, nh, ch)[0, 0]          # [ncal][nh][64]
+    pos = synth.calibration_positions(g, ncal, 1024)
+    X = np.empty((nh, ncal, 64), np.float32)
+    for h in range(nh):
+        for i in range(ncal):
+            X[h, i] = oracle.rope_apply(keys[i, h], int(pos[i]), cs)
+    pi, sg = tq.calibrate_rotation(torch.from_numpy(X).cuda())
+    pi = pi.cpu().numpy().astype(np.float64)
+    sg = sg.cpu().numpy().astype(np.float64)
+    for h in range(nh):
+        P = pi[h]
+        ref_pi, ref_s = oracle.calibrate_rotation(X[h])
+        np.testing.assert_allclose(sg[h], ref_s, rtol=1e-5)
+        np.testing.assert_allclose(P @ P.T, np.eye(64), atol=1e-6)
+        G = X[h].astype(np.float64).T @ X[h].astype(np.float64)
+        Dg = P @ G @ P.T
+        assert np.max(np.abs(Dg - np.diag(np.diag(Dg)))) <= 1e-5 * ref_s[0] ** 2
+        # rows with a well separated singular value match the oracle's row
+        gap = np.minimum(np.abs(np.diff(np.concatenate(([np.inf], ref_s)))),
+                         np.abs(np.diff(np.concatenate((ref_s, [-np.inf])))))
+        sep = gap > 1e-3 * ref_s[0]
+        np.testing.assert_allclose(P[sep], ref_pi[sep].astype(np.float64), atol=1e-4)
