@@ -28,11 +28,14 @@
  *     nibble at bits 4*(i%8) .. 4*(i%8)+3 of 32-bit word i/8 (little endian).
  *     Nibble = idx | (sign << 3): idx is the 3-bit LUT index, sign the QJL bit
  *     (K always; V only with TQ_V_QJL, else 0).
- *   - tile interleaving: slots are grouped in tiles of 64. For slot s of a
- *     (layer, head) region, tile t = s/64, lane r = s%64, the 16-byte half c
- *     (c = 0: words 0-3, c = 1: words 4-7) lives at byte
- *         region_base + t*2048 + (c*64 + r)*16
- *     in k_codes (and likewise v_codes), region_base = (l*H + h)*slots*32.
+ *   - tiles: slots are grouped in tiles of 64; a tile holds 2048 bytes of
+ *     k_codes and 2048 bytes of v_codes. Region (l, h) starts at byte
+ *     (l*H + h)*slots*32 of each plane; slot s is in tile t = s/64 at r = s%64.
+ *     K plane, token-major: the 16-byte half c (words 4c..4c+3, codes
+ *       32c..32c+31) of slot s is at byte t*2048 + (c*64 + r)*16.
+ *     V plane, dimension-major: for dimension i, the codes of the tile's 64
+ *       slots form 32 bytes; half c (slots 32c..32c+31) is at byte
+ *       t*2048 + (c*64 + i)*16, and slot r is nibble r%8 of word (r%32)/8.
  *   - scalars: 4 fp16 values per slot at byte (l*H + h)*slots*8 + s*8:
  *         [0] n_k  = ||k^||,  [1] g_k = ||r_k|| (QJL residual norm),
  *         [2] n_v  = ||v^||,  [3] g_v = ||r_v|| (0 unless TQ_V_QJL).

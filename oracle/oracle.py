@@ -70,6 +70,8 @@ def lib():
         L.orc_quantize_vector.argtypes = [P, P, P, i32, P, P, P]
         L.orc_pack_slot.argtypes = [P, i64, P]
         L.orc_unpack_slot.argtypes = [P, i64, P]
+        L.orc_pack_slot_v.argtypes = [P, i64, P]
+        L.orc_unpack_slot_v.argtypes = [P, i64, P]
         L.orc_quantize_pack.argtypes = [i32, i32, i64, u32, P, i32, P, P, i32, i32,
                                         i32, i32, P, P, P, P, P, P, P, P, P]
         L.orc_decode.argtypes = [i32, i32, i64, u32, dbl, P, i32, P, i32, i32, i32,
@@ -149,13 +151,17 @@ def quantize_vector(xhat, lut, S, sign_mode=SIGN_PROJECTED):
     return nib, n16.value, g16.value
 
 
-def pack_slot(region: np.ndarray, slot: int, nib) -> None:
-    lib().orc_pack_slot(_p(region), int(slot), _p(np.ascontiguousarray(nib, np.uint8)))
+def pack_slot(region: np.ndarray, slot: int, nib, plane: str = "k") -> None:
+    """Write one slot's 64 nibbles into a (layer, head) region of the K plane
+    (token-major tiles) or the V plane (dimension-major tiles)."""
+    f = lib().orc_pack_slot if plane == "k" else lib().orc_pack_slot_v
+    f(_p(region), int(slot), _p(np.ascontiguousarray(nib, np.uint8)))
 
 
-def unpack_slot(region: np.ndarray, slot: int) -> np.ndarray:
+def unpack_slot(region: np.ndarray, slot: int, plane: str = "k") -> np.ndarray:
     nib = np.empty(D, dtype=np.uint8)
-    lib().orc_unpack_slot(_p(np.ascontiguousarray(region)), int(slot), _p(nib))
+    f = lib().orc_unpack_slot if plane == "k" else lib().orc_unpack_slot_v
+    f(_p(np.ascontiguousarray(region)), int(slot), _p(nib))
     return nib
 
 

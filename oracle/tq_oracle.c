@@ -16,7 +16,8 @@
  *     evaluation order: sequential fmaf chains, correctly rounded sqrtf and
  *     division. Build with -ffp-contract=off so nothing else is fused.
  *   - Packing into the cache layout (Sec. 4.2 packs 8 codes per 32-bit word;
- *     here each code is a 4-bit nibble that also holds the sign bit).
+ *     here each code is a 4-bit nibble that also holds the sign bit; key
+ *     tiles are token-major, value tiles dimension-major).
  *   - Decode attention (Sec. 3.1 decode steps; Algorithm 1 of Sec. 4.3),
  *     fp64: a streaming online-softmax form and a two-step form that first
  *     materializes the dequantized keys and values.
@@ -214,18 +215,19 @@ void orc_quantize_vector(const float* xhat, const float* c, const float* S,
 /* 32-bit container); 64-slot tiles, 16-byte halves interleaved by slot.     */
 /* ------------------------------------------------------------------------ */
 
-/* Byte offset of 16-byte half `c` of slot s inside one (layer, head) region. */
-static int64_t half_offset(int64_t s, int c) {
+/* K plane, token-major tiles: 16-byte half c (codes 32c..32c+31) of slot s
+ * sits at tile*2048 + (c*64 + s%64)*16 inside one (layer, head) region. */
+static int64_t k_half_offset(int64_t s, int c) {
   int64_t tile = s / TILE, lane = s % TILE;
   return tile * (TILE * 32) + ((int64_t)c * TILE + lane) * 16;
 }
 
-/* Write the 64 nibbles of one slot. */
+/* Write the 64 nibbles of one slot of the K plane. */
 void orc_pack_slot(uint8_t* region, int64_t s, const uint8_t* nib) {
   for (int w = 0; w < 8; ++w) {
     uint32_t word = 0;
     for (int j = 0; j < 8; ++j) word |= (uint32_t)(nib[w * 8 + j] & 0xF) << (4 * j);
-    uint8_t* dst = region + half_offset(s, w / 4) + (w % 4) * 4;
+    uint8_t* dst = region + k_half_offset(s, w / 4) + (w % 4) * 4;
     dst[0] = (uint8_t)(word & 0xFF);
     dst[1] = (uint8_t)((word >> 8) & 0xFF);
     dst[2] = (uint8_t)((word >> 16) & 0xFF);
@@ -233,13 +235,44 @@ void orc_pack_slot(uint8_t* region, int64_t s, const uint8_t* nib) {
   }
 }
 
-/* Read the 64 nibbles of one slot. */
+/* Read the 64 nibbles of one slot of the K plane. */
 void orc_unpack_slot(const uint8_t* region, int64_t s, uint8_t* nib) {
   for (int w = 0; w < 8; ++w) {
-    const uint8_t* src = region + half_offset(s, w / 4) + (w % 4) * 4;
+    const uint8_t* src = region + k_half_offset(s, w / 4) + (w % 4) * 4;
     uint32_t word = (uint32_t)src[0] | ((uint32_t)src[1] << 8) |
                     ((uint32_t)src[2] << 16) | ((uint32_t)src[3] << 24);
     for (int j = 0; j < 8; ++j) nib[w * 8 + j] = (uint8_t)((word >> (4 * j)) & 0xF);
+  }
+}
+
+/* V plane, dimension-major tiles: for dimension i the 64 slots of a tile
+ * form 32 bytes; 16-byte half c (slots 32c..32c+31 of the tile) sits at
+ * tile*2048 + (c*64 + i)*16, and slot r of the tile is nibble r%8 of 32-bit
+ * word (r%32)/8 of that half. Returns the byte holding the nibble and its
+ * bit offset inside that byte (0 or 4). */
+static int64_t v_nibble_byte(int64_t s, int i, int* shift) {
+  int64_t tile = s / TILE;
+  int r = (int)(s % TILE);
+  int c = r / 32, w = (r % 32) / 8, j = r % 8;
+  *shift = (j % 2) * 4;
+  return tile * (TILE * 32) + ((int64_t)c * TILE + i) * 16 + w * 4 + j / 2;
+}
+
+/* Write the 64 nibbles of one slot of the V plane (other slots untouched). */
+void orc_pack_slot_v(uint8_t* region, int64_t s, const uint8_t* nib) {
+  for (int i = 0; i < D; ++i) {
+    int sh;
+    int64_t off = v_nibble_byte(s, i, &sh);
+    region[off] = (uint8_t)((region[off] & ~(0xF << sh)) | ((nib[i] & 0xF) << sh));
+  }
+}
+
+/* Read the 64 nibbles of one slot of the V plane. */
+void orc_unpack_slot_v(const uint8_t* region, int64_t s, uint8_t* nib) {
+  for (int i = 0; i < D; ++i) {
+    int sh;
+    int64_t off = v_nibble_byte(s, i, &sh);
+    nib[i] = (uint8_t)((region[off] >> sh) & 0xF);
   }
 }
 
@@ -290,7 +323,7 @@ void orc_quantize_pack(int L, int H, int64_t slots, uint32_t flags,
           orc_quantize_vector(vh, lut_v + ((size_t)l * H + h) * 8, S, vsign, vn, &nv, &gv);
           int64_t region = ((int64_t)l * H + h) * slots;
           orc_pack_slot(kc + region * 32, s, kn);
-          orc_pack_slot(vc + region * 32, s, vn);
+          orc_pack_slot_v(vc + region * 32, s, vn);
           uint16_t* dst = sc + (region + s) * 4;
           dst[0] = nk; dst[1] = gk; dst[2] = nv; dst[3] = gv;
         }
@@ -377,7 +410,7 @@ static void decode_unit_streaming(const unit_ctx* u, uint32_t flags, double scal
     int64_t s = s0 + j;
     uint8_t kn[D], vn[D];
     orc_unpack_slot(kreg, s, kn);
-    orc_unpack_slot(vreg, s, vn);
+    orc_unpack_slot_v(vreg, s, vn);
     const uint16_t* sc = screg + s * 4;
     double nk = orc_f16_to_f32(sc[0]), gk = orc_f16_to_f32(sc[1]);
     double nv = orc_f16_to_f32(sc[2]), gv = orc_f16_to_f32(sc[3]);
@@ -410,7 +443,7 @@ static void decode_unit_twostep(const unit_ctx* u, uint32_t flags, double scale,
     int64_t s = s0 + j;
     uint8_t kn[D], vn[D];
     orc_unpack_slot(kreg, s, kn);
-    orc_unpack_slot(vreg, s, vn);
+    orc_unpack_slot_v(vreg, s, vn);
     const uint16_t* sc = screg + s * 4;
     logits[j] = key_score(kn, orc_f16_to_f32(sc[0]), orc_f16_to_f32(sc[1]), u, flags) * scale;
     dequant_v(vn, orc_f16_to_f32(sc[2]), orc_f16_to_f32(sc[3]), u->cv, flags,

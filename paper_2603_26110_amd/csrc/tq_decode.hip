@@ -271,35 +271,44 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a, int64_t total
   }
 
   if (participants > 1) {
+    // Publish this split's partial with agent-scope (coherent) stores and wait
+    // until they are performed before counting the split in; the last split
+    // reads the partials back with agent-scope loads. No block writes back or
+    // invalidates the L2 (which a device-wide fence would do on every block).
     float* part = a.partials + (unit * a.nsplit + split) * kPartialFloats;
     if (t < kDim) {
-      part[4 + t] = O;
-      if (VQJL) part[4 + kDim + t] = SG;
-      if (t == 0) { part[0] = M; part[1] = L; }
+      __hip_atomic_store(part + 4 + t, O, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (VQJL) __hip_atomic_store(part + 4 + kDim + t, SG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (t == 0) {
+        __hip_atomic_store(part + 0, M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(part + 1, L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
-    __threadfence();
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (t == 0) {
-      const uint32_t prev = atomicAdd(a.counters + unit, 1u);
+      const uint32_t prev = __hip_atomic_fetch_add(a.counters + unit, 1u, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT);
       sm.last = (prev == (uint32_t)(participants - 1)) ? 1 : 0;
     }
     __syncthreads();
     if (!sm.last) return;
-    __threadfence();
     if (t < kDim) {
-      const float* base = a.partials + unit * a.nsplit * kPartialFloats;
+      float* base = a.partials + unit * a.nsplit * kPartialFloats;
       M = -INFINITY;
-      for (int s = 0; s < participants; ++s) M = fmaxf(M, base[s * kPartialFloats]);
+      for (int s = 0; s < participants; ++s)
+        M = fmaxf(M, __hip_atomic_load(base + s * kPartialFloats, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
       L = 0.0f; O = 0.0f; SG = 0.0f;
       for (int s = 0; s < participants; ++s) {
-        const float* ps = base + s * kPartialFloats;
-        const float f = exp2f(ps[0] - M);
-        L += ps[1] * f;
-        O += ps[4 + t] * f;
-        if (VQJL) SG += ps[4 + kDim + t] * f;
+        float* ps = base + s * kPartialFloats;
+        const float f = exp2f(__hip_atomic_load(ps, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - M);
+        L += __hip_atomic_load(ps + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
+        O += __hip_atomic_load(ps + 4 + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
+        if (VQJL) SG += __hip_atomic_load(ps + 4 + kDim + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
       }
     }
-    if (t == 0) a.counters[unit] = 0u;   // leave the workspace zeroed
+    // leave the workspace zeroed for the next call
+    if (t == 0) __hip_atomic_store(a.counters + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
   // ---------------------------------------------------------------- epilogue

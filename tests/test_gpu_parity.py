@@ -30,11 +30,15 @@ def test_library_loaded_and_version():
 
 
 def test_rope_table_matches_oracle():
+    # fp64 cos/sin on the GPU and in libm may differ in the last fp64 bits;
+    # after rounding to fp32 the tables agree to within one fp32 ulp.
     cs = tq.rope_table(8256).cpu().numpy()
     ref = oracle.rope_table(8256)
-    diff = np.abs(cs.astype(np.float64) - ref)
-    ulp = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64)
-    assert np.all(diff <= ulp)
+    ia = cs.view(np.int32).astype(np.int64)
+    ib = ref.view(np.int32).astype(np.int64)
+    same_sign = np.sign(cs) == np.sign(ref)
+    ulps = np.where(same_sign, np.abs(ia - ib), np.abs(ia) + np.abs(ib))
+    assert np.max(ulps) <= 1
     assert np.mean(cs == ref) > 0.999
 
 
@@ -131,8 +135,8 @@ def test_quantize_end_to_end_matches_up_to_threshold_rounding(T):
             s = int(case.slot0[b]) + j
             for h in range(H):
                 for is_key, which in ((True, "k"), (False, "v")):
-                    ng_ = oracle.unpack_slot(got.region(which, 0, h), s)
-                    no_ = oracle.unpack_slot(oc.region(which, 0, h), s)
+                    ng_ = oracle.unpack_slot(got.region(which, 0, h), s, which)
+                    no_ = oracle.unpack_slot(oc.region(which, 0, h), s, which)
                     total += 64
                     bad = (ng_ & 7) != (no_ & 7)
                     sign_diff += int(((ng_ >> 3) != (no_ >> 3)).sum())

@@ -55,7 +55,7 @@ def build(g, n, L=1, H=1, slots=None, flags=oracle.V_ROTATE, lut=LUT32, S=None, 
 
 
 def dequant_v_unrotated(cache, l, h, s, lut):
-    nib = oracle.unpack_slot(cache.region("v", l, h), s)
+    nib = oracle.unpack_slot(cache.region("v", l, h), s, "v")
     nv = float(np.uint16(cache.scalars(l, h)[s, 2]).view(np.float16))
     return nv / 8.0 * lut[nib & 7].astype(np.float64)
 

@@ -194,6 +194,49 @@ def test_pack_matches_vectorized_shift_sum_and_round_trips():
         np.testing.assert_array_equal(oracle.unpack_slot(region, s), allnib[s])
 
 
+def test_v_plane_layout_hand_worked():
+    # V tiles are dimension-major. Slot 70 = tile 1, slot-in-tile 6: half 0,
+    # word 0, nibble 6 -> bits 24..27. Dimension 5 of that half is the 16-byte
+    # row at 2048 + (0*64 + 5)*16 = 2128, so the nibble is the low half of byte
+    # 2128 + 3.
+    region = np.zeros(4096, np.uint8)
+    nib = np.zeros(64, np.uint8)
+    nib[5] = 0x9
+    oracle.pack_slot(region, 70, nib, "v")
+    assert np.flatnonzero(region).tolist() == [2131] and region[2131] == 0x09
+    # slot 127 = tile 1, slot 63: half 1, word 3, nibble 7 -> high half of
+    # byte 3 of word 3 of dimension 63's row at 2048 + (64 + 63)*16 = 4080
+    region[:] = 0
+    nib[:] = 0
+    nib[63] = 0xE
+    oracle.pack_slot(region, 127, nib, "v")
+    assert np.flatnonzero(region).tolist() == [4080 + 12 + 3] and region[4095] == 0xE0
+
+
+def test_v_plane_matches_transposed_construction_and_round_trips():
+    # Independent construction: for each dimension, the tile's 64 slot codes
+    # packed 8 per 32-bit word (shift-sum), two 16-byte halves per dimension.
+    g = synth.rng(9)
+    slots = 128
+    region = np.zeros(slots * 32, np.uint8)
+    allnib = g.integers(0, 16, (slots, 64)).astype(np.uint8)
+    for s in g.permutation(slots):               # any write order
+        oracle.pack_slot(region, int(s), allnib[s], "v")
+    ref = np.zeros(slots * 32, np.uint8)
+    for t in range(slots // 64):
+        tile = allnib[64 * t:64 * t + 64]        # [slot][dim]
+        for i in range(64):
+            col = tile[:, i].astype(np.uint32).reshape(8, 8)
+            words = (col << (4 * np.arange(8, dtype=np.uint32))).sum(-1)
+            wb = words.astype("<u4").view(np.uint8).reshape(2, 16)
+            for c in range(2):
+                off = t * 2048 + (c * 64 + i) * 16
+                ref[off:off + 16] = wb[c]
+    np.testing.assert_array_equal(region, ref)
+    for s in [0, 5, 63, 64, 127]:
+        np.testing.assert_array_equal(oracle.unpack_slot(region, s, "v"), allnib[s])
+
+
 def test_quantize_pack_writes_expected_slots_and_skips_out_of_range():
     g = synth.rng(7)
     L, H, B, T = 2, 3, 2, 5
@@ -222,7 +265,7 @@ def test_quantize_pack_writes_expected_slots_and_skips_out_of_range():
             assert sc[j, 0] == n16 and sc[j, 1] == g16
             vh = oracle.rotated_input(v[0, 0, j, h], False, 3 + j, cs, pi[1, h])
             nibv, nv16, gv16 = oracle.quantize_vector(vh, LUT32, S, oracle.SIGN_NONE)
-            np.testing.assert_array_equal(oracle.unpack_slot(cache.region("v", 1, h), j), nibv)
+            np.testing.assert_array_equal(oracle.unpack_slot(cache.region("v", 1, h), j, "v"), nibv)
             assert sc[j, 2] == nv16 and sc[j, 3] == 0
 
 
@@ -247,5 +290,5 @@ def test_quantize_pack_sign_modes(flags, kmode, vmode):
                                   rotate_v=bool(flags & oracle.V_ROTATE))
         np.testing.assert_array_equal(oracle.unpack_slot(cache.region("k", 0, 0), j),
                                       oracle.quantize_vector(kh, LUT32, S, kmode)[0])
-        np.testing.assert_array_equal(oracle.unpack_slot(cache.region("v", 0, 0), j),
+        np.testing.assert_array_equal(oracle.unpack_slot(cache.region("v", 0, 0), j, "v"),
                                       oracle.quantize_vector(vh, LUT32, S, vmode)[0])
