@@ -36,6 +36,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="esm2-650m-33layer-seq1024")
     ap.add_argument("--replica-bytes", type=float, default=1.1 * 2 ** 30)
+    ap.add_argument("--replicas", type=int, default=0,
+                    help="number of input replicas (default: enough for --replica-bytes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0,
@@ -101,7 +103,7 @@ def main():
     q_d = t_(q)
     per_replica = (tq.cache_bytes(L, H, slots) + pi_d.numel() * 4 + 2 * q_d.numel() * q_d.element_size()
                    + 2 * k_new.numel() * k_new.element_size())
-    R = max(2, math.ceil(args.replica_bytes / per_replica))
+    R = args.replicas if args.replicas > 0 else max(2, math.ceil(args.replica_bytes / per_replica))
     reps = []
     for r in range(R):
         c = tq.Cache(L, H, slots, device=dev)

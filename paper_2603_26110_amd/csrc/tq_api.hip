@@ -104,6 +104,8 @@ tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache, const
     return fail(TQ_ERR_ARG, "too many token-heads");
   if ((int64_t)B * params->num_heads > 65535 || nlayers > 65535)
     return fail(TQ_ERR_ARG, "B*H and nlayers must be <= 65535");
+  if (T < 64 && (int64_t)nlayers * B * T * params->num_heads >= ((int64_t)1 << 31))
+    return fail(TQ_ERR_ARG, "too many token-heads for one call");
   tq::QuantArgs a{};
   a.k = k; a.v = v;
   a.B = B; a.T = T; a.H = params->num_heads; a.layer0 = layer0; a.nlayers = nlayers;
@@ -119,8 +121,8 @@ tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache, const
 size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B, int32_t nlayers, int32_t max_len) {
   if (!params || params->num_heads <= 0 || B <= 0 || nlayers <= 0 || max_len < 0) return 0;
   const int64_t units = (int64_t)nlayers * B * params->num_heads;
-  int nsplit, split_tiles;
-  tq::decode_plan((int)std::min<int64_t>(units, 1 << 30), max_len, &nsplit, &split_tiles);
+  int waves, nsplit, split_tiles;
+  tq::decode_plan((int)std::min<int64_t>(units, 1 << 30), max_len, &waves, &nsplit, &split_tiles);
   if (nsplit <= 1) return 0;
   const size_t part = (size_t)units * nsplit * tq::kPartialFloats * sizeof(float);
   const size_t cnt = (size_t)units * sizeof(uint32_t);
@@ -149,8 +151,8 @@ tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const
   if ((int64_t)max_len > cache->slots) return fail(TQ_ERR_CAPACITY, "max_len exceeds the cache slots");
   const int64_t units = (int64_t)nlayers * B * params->num_heads;
   if (units >= ((int64_t)1 << 31)) return fail(TQ_ERR_ARG, "too many (layer, sequence, head) units");
-  int nsplit, split_tiles;
-  tq::decode_plan((int)units, max_len, &nsplit, &split_tiles);
+  int waves, nsplit, split_tiles;
+  tq::decode_plan((int)units, max_len, &waves, &nsplit, &split_tiles);
   const size_t need = tq_decode_workspace_bytes(params, B, nlayers, max_len);
   if (need > 0) {
     if (!workspace) return fail(TQ_ERR_CAPACITY, "workspace of %zu bytes required", need);
@@ -178,7 +180,7 @@ tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const
     a.partials = (float*)workspace;
     a.counters = (uint32_t*)((char*)workspace + ((part + 255) / 256) * 256);
   }
-  return hip_status(tq::launch_decode(a, (hipStream_t)stream), "tq_decode_attend launch");
+  return hip_status(tq::launch_decode(a, waves, (hipStream_t)stream), "tq_decode_attend launch");
 }
 
 tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal, float* pi_out,

@@ -1,50 +1,60 @@
 // Fused decode attention over the packed 3-bit cache (TurboESM Sec. 3.1
 // decode steps 1-4; Algorithm 1 of Sec. 4.3).
 //
-// One block (4 waves) handles one (sequence, layer, head) unit, or one split
-// of its 64-token tiles. Per block:
+// One block (WAVES waves) handles one (sequence, layer, head) unit, or one
+// split of its 64-token tiles. Per block:
+//   loads     the first tile of every wave, this thread's slice of Pi (and of
+//             S), the query and the tables are requested before any
+//             arithmetic, so the prologue runs under the HBM latency.
 //   prologue  q' = RoPE(q), q^ = Pi q', u = S q^ (or q^ for the per-element
 //             residual form), and a 64 x 16 LDS table
 //             T[i][nibble] = (q^_i c_K[nibble & 7], +-u_i)
 //             so one table read per code gives both score terms. Rotating the
 //             query once replaces the per-key inverse rotation of Algorithm 1
 //             (identical by Eq. 4).
-//   main loop each wave takes 64-token tiles. Keys are scored one lane per
-//             token: score = n_k/8 (sum_i T_A + coef sum_i T_B), coef = alpha g_k
-//             (QJL) or ebar_K. Online softmax in base 2 with a wave-uniform
-//             running max that is raised only when a tile max exceeds it by
-//             more than 2^8 (rescaling is rare). Values are accumulated one
-//             lane per dimension from the dimension-major V tile, with the
-//             tile's token weights broadcast through LDS.
+//   main loop each wave takes 64-token tiles and keeps the next few in flight.
+//             Keys are scored one lane per token:
+//             score = n_k/8 (sum_i T_A + coef sum_i T_B), coef = alpha g_k (QJL)
+//             or ebar_K. Online softmax in base 2 with a wave-uniform running
+//             max that is raised only when a tile max exceeds it by more than
+//             2^8 (rescaling is rare). Values are accumulated one lane per
+//             dimension from the dimension-major V tile, with the tile's token
+//             weights broadcast through LDS.
 //   merge     waves merge through LDS; splits of a unit merge through a
-//             workspace of (m, l, o) partials: the last block of the unit to
-//             finish (atomic counter) combines them by log-sum-exp.
-//   epilogue  o = Pi^T (o^ / l) (one inverse rotation), plus the V residual
-//             estimate alpha S^T s or ebar_V s when V carries sign bits.
-// Work items are mapped so that all splits of a unit land on one XCD
-// (blocks are dealt to the 8 XCDs round-robin), keeping Pi in that XCD's L2.
+//             workspace of (m, l, o) partials written and read with
+//             agent-scope atomics: the last split to finish (atomic counter)
+//             combines them by log-sum-exp.
+//   epilogue  o = Pi^T (o^ / l) (one inverse rotation; Pi staged in LDS), plus
+//             the V residual estimate alpha S^T s or ebar_V s when V carries
+//             sign bits.
+// Work items are dealt so that all splits of a unit land on one XCD (blocks
+// go to the 8 XCDs round-robin), keeping that unit's Pi in one L2.
+#include <stdlib.h>
+
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
 
 namespace tq {
 
-constexpr int kWaves = 4;
 constexpr float kLazyRescale = 8.0f;   // log2 headroom before the max is raised
 constexpr int kXcds = 8;
+constexpr int kPiPitch = kDim + 1;     // padded LDS row of Pi (conflict-free columns)
 
+template <int WAVES>
 struct DecodeSmem {
   float2 ktab[kDim * 16];
+  float pi[kDim * kPiPitch];
   float vtab[16];
   float q[kDim];
   float qh[kDim];
   float u[kDim];
-  float part[kWaves][kDim];
-  float wp[kWaves][kDim];    // per-tile token weights (V accumulate)
-  float wg[kWaves][kDim];    // per-tile token weights for the V residual term
-  float wo[kWaves][kDim];
-  float wsg[kWaves][kDim];
-  float wm[kWaves];
-  float wl[kWaves];
+  float part[WAVES][kDim];
+  float wp[WAVES][kDim];        // per-tile token weights (V accumulate)
+  float wg[WAVES][kDim];        // per-tile token weights for the V residual term
+  float wo[WAVES][kDim];
+  float wsg[WAVES][kDim];
+  float wm[WAVES];
+  float wl[WAVES];
   float oh[kDim];
   float sh[kDim];
   int last;
@@ -56,43 +66,75 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// y = M x for a 64 x 64 row-major global matrix, x in LDS; all 256 threads.
-// Thread t sums columns 16*(t/64) .. +15 of row t%64; partials go to `part`.
-__device__ __forceinline__ float matvec_rows(const float* M, const float* x, DecodeSmem& sm) {
-  const int t = threadIdx.x, i = t & 63, q4 = t >> 6;
-  const float4* row = reinterpret_cast<const float4*>(M + i * kDim + q4 * 16);
-  float acc = 0.0f;
-#pragma unroll
-  for (int k4 = 0; k4 < 4; ++k4) {
-    const float4 m = row[k4];
-    acc = fmaf(m.x, x[q4 * 16 + 4 * k4 + 0], acc);
-    acc = fmaf(m.y, x[q4 * 16 + 4 * k4 + 1], acc);
-    acc = fmaf(m.z, x[q4 * 16 + 4 * k4 + 2], acc);
-    acc = fmaf(m.w, x[q4 * 16 + 4 * k4 + 3], acc);
+// (byte B of x) & m, one VALU op (sub-dword operand select).
+template <int B>
+__device__ __forceinline__ uint32_t and_byte(uint32_t m, uint32_t x) {
+  uint32_t r;
+  if constexpr (B == 0) {
+    r = x & m;
+  } else if constexpr (B == 1) {
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+        : "=v"(r) : "v"(m), "v"(x));
+  } else if constexpr (B == 2) {
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2"
+        : "=v"(r) : "v"(m), "v"(x));
+  } else {
+    asm("v_and_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+        : "=v"(r) : "v"(m), "v"(x));
   }
-  sm.part[q4][i] = acc;
-  __syncthreads();
-  float y = 0.0f;
-  if (t < kDim) y = (sm.part[0][t] + sm.part[1][t]) + (sm.part[2][t] + sm.part[3][t]);
-  __syncthreads();
-  return y;   // valid in threads 0..63
+  return r;
 }
 
-// y = M^T x (y_k = sum_i M[i][k] x_i); coalesced row reads; all 256 threads.
-__device__ __forceinline__ float matvec_cols(const float* M, const float* x, DecodeSmem& sm) {
-  const int t = threadIdx.x, k = t & 63, q4 = t >> 6;
-  float acc = 0.0f;
-#pragma unroll
-  for (int ii = 0; ii < 16; ++ii) {
-    const int i = q4 * 16 + ii;
-    acc = fmaf(M[i * kDim + k], x[i], acc);
-  }
-  sm.part[q4][k] = acc;
-  __syncthreads();
-  float y = 0.0f;
-  if (t < kDim) y = (sm.part[0][t] + sm.part[1][t]) + (sm.part[2][t] + sm.part[3][t]);
-  __syncthreads();
-  return y;
+// Byte offsets of the 8 nibbles of x into a table with 8-byte entries indexed
+// by the nibble: nibble 2b comes from byte b of x << 3, nibble 2b+1 from byte
+// b of x >> 1 (each masked with 0x78 = nibble * 8).
+__device__ __forceinline__ void nibble_offsets8(uint32_t x, uint32_t (&off)[8]) {
+  const uint32_t m = 0x78u;
+  const uint32_t lo = x << 3, hi = x >> 1;
+  off[0] = and_byte<0>(m, lo); off[1] = and_byte<0>(m, hi);
+  off[2] = and_byte<1>(m, lo); off[3] = and_byte<1>(m, hi);
+  off[4] = and_byte<2>(m, lo); off[5] = and_byte<2>(m, hi);
+  off[6] = and_byte<3>(m, lo); off[7] = and_byte<3>(m, hi);
+}
+
+// Byte offsets (nibble & 7) * 4 of the 8 nibbles of x into a float table:
+// nibble 2b from byte b of x << 2, nibble 2b+1 from byte b of x >> 2 (0x1C).
+__device__ __forceinline__ void nibble_offsets4(uint32_t x, uint32_t (&off)[8]) {
+  const uint32_t m = 0x1Cu;
+  const uint32_t lo = x << 2, hi = x >> 2;
+  off[0] = and_byte<0>(m, lo); off[1] = and_byte<0>(m, hi);
+  off[2] = and_byte<1>(m, lo); off[3] = and_byte<1>(m, hi);
+  off[4] = and_byte<2>(m, lo); off[5] = and_byte<2>(m, hi);
+  off[6] = and_byte<3>(m, lo); off[7] = and_byte<3>(m, hi);
+}
+
+// Wave-wide reductions: 16-lane rows through DPP, then the four rows via
+// readlane (the result is wave-uniform).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float wave_max_uniform(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));    // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp<0x4E>(v));    // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp<0x141>(v));   // row_half_mirror
+  v = fmaxf(v, dpp<0x140>(v));   // row_mirror
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return fmaxf(fmaxf(a, b), fmaxf(c, d));
+}
+__device__ __forceinline__ float wave_sum_uniform(float v) {
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  v += dpp<0x141>(v);
+  v += dpp<0x140>(v);
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+  return (a + b) + (c + d);
 }
 
 __device__ __forceinline__ void store_out(const DecodeArgs& a, int64_t unit, int k, float v) {
@@ -102,21 +144,52 @@ __device__ __forceinline__ void store_out(const DecodeArgs& a, int64_t unit, int
     reinterpret_cast<float*>(a.out)[unit * kDim + k] = v;
 }
 
-template <bool VQJL>
-__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a, int64_t total_work,
-                                                     int64_t per_xcd) {
-  __shared__ DecodeSmem sm;
-  const int64_t bid = blockIdx.x;
-  const int64_t work = (bid % kXcds) * per_xcd + bid / kXcds;
+struct TileRegs {
+  uint4 k0, k1, v0, v1;
+  uint2 sc;
+};
+
+__device__ __forceinline__ void load_tile(TileRegs& r, const uint8_t* kreg, const uint8_t* vreg,
+                                          const uint2* sreg, int64_t gt, int64_t s0, int tt,
+                                          int lane) {
+  r.k0 = *reinterpret_cast<const uint4*>(kreg + tile_half_offset(gt, 0, lane));
+  r.k1 = *reinterpret_cast<const uint4*>(kreg + tile_half_offset(gt, 1, lane));
+  r.v0 = *reinterpret_cast<const uint4*>(vreg + tile_half_offset(gt, 0, lane));
+  r.v1 = *reinterpret_cast<const uint4*>(vreg + tile_half_offset(gt, 1, lane));
+  r.sc = sreg[s0 + (int64_t)tt * kTile + lane];
+}
+
+// Sum of T[i][nibble_i] over the 8 codes of word w (dims 8w..8w+7).
+__device__ __forceinline__ void score_word(const float2* ktab_w, uint32_t x, float& A, float& B) {
+  uint32_t off[8];
+  nibble_offsets8(x, off);
+  const char* base = reinterpret_cast<const char*>(ktab_w);
+  float2 e[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) e[j] = *reinterpret_cast<const float2*>(base + j * 128 + off[j]);
+  A += ((e[0].x + e[1].x) + (e[2].x + e[3].x)) + ((e[4].x + e[5].x) + (e[6].x + e[7].x));
+  B += ((e[0].y + e[1].y) + (e[2].y + e[3].y)) + ((e[4].y + e[5].y) + (e[6].y + e[7].y));
+}
+
+template <int WAVES, bool VQJL>
+__global__ __launch_bounds__(WAVES * 64)
+__attribute__((amdgpu_waves_per_eu((WAVES == 8 && !VQJL) ? 6 : 1)))
+void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
+  constexpr int NT = WAVES * 64;
+  constexpr int COLS = kDim / WAVES;       // columns of Pi / S per thread
+  __shared__ DecodeSmem<WAVES> sm;
+  const int bid = blockIdx.x;
+  const int work = (bid % kXcds) * per_xcd + bid / kXcds;
   if (work >= total_work) return;
-  const int64_t unit = work / a.nsplit;
-  const int split = (int)(work % a.nsplit);
-  const int h = (int)(unit % a.H);
-  const int b = (int)((unit / a.H) % a.B);
-  const int li = (int)(unit / ((int64_t)a.H * a.B));
+  const int unit = work / a.nsplit;
+  const int split = work - unit * a.nsplit;
+  const int h = unit % a.H;
+  const int b = (unit / a.H) % a.B;
+  const int li = unit / (a.H * a.B);
   const int l = a.layer0 + li;
-  const int64_t lh = (int64_t)l * a.H + h;
-  const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+  const int lh = l * a.H + h;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
 
   const int n = a.seq_len[b];
   const int64_t s0 = a.seq_slot0[b];
@@ -132,138 +205,218 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a, int64_t total
   if (tile_begin >= ntiles) return;
   const int tile_end = min(ntiles, tile_begin + a.split_tiles);
   const int participants = (ntiles + a.split_tiles - 1) / a.split_tiles;
-
-  const float* pi_lh = a.pi + lh * kDim * kDim;
   const bool paper = (a.flags & kQjlPaper) != 0;
 
-  // ---------------------------------------------------------------- prologue
+  // ------------------------------------------------------------------ loads
+  const uint8_t* kreg = a.k_codes + (int64_t)lh * a.slots * 32;
+  const uint8_t* vreg = a.v_codes + (int64_t)lh * a.slots * 32;
+  const uint2* sreg = reinterpret_cast<const uint2*>(a.scalars + (int64_t)lh * a.slots * 4);
+  const int64_t tile0 = s0 >> 6;
+  const int ri = t & 63, cq = t >> 6;      // row and column group of Pi / S
+  const float4* pi_row = reinterpret_cast<const float4*>(a.pi + (int64_t)lh * kDim * kDim + ri * kDim + cq * COLS);
+  float4 pr[COLS / 4];
+#pragma unroll
+  for (int k = 0; k < COLS / 4; ++k) pr[k] = pi_row[k];
+  float4 sr[COLS / 4];
+  if (!paper) {
+    const float4* s_row = reinterpret_cast<const float4*>(a.qjl_s + ri * kDim + cq * COLS);
+#pragma unroll
+    for (int k = 0; k < COLS / 4; ++k) sr[k] = s_row[k];
+  }
+  float qv = 0.0f;
+  float2 cs = make_float2(1.0f, 0.0f);
+  const bool half = (a.flags & kRopeHalf) != 0;
   if (t < kDim) {
-    const float qv = load_in(a.q, unit * kDim + t, a.f16_in != 0);
-    const bool half = (a.flags & kRopeHalf) != 0;
+    qv = load_in(a.q, (int64_t)unit * kDim + t, a.f16_in != 0);
+    const int m = half ? (t & 31) : (t >> 1);
+    cs = reinterpret_cast<const float2*>(a.rope_cs + (int64_t)qp * 2 * kPairs)[m];
+  }
+  const float ck = a.lut_k[lh * 8 + (t & 7)];
+  const float cvv = a.lut_v[lh * 8 + (t & 7)];
+  const float ebar_k = paper ? a.ebar[lh * 2 + 0] : 0.0f;
+
+  // Tiles are requested after Pi, S and the query (the prologue needs those
+  // first). Each wave keeps DEPTH tiles in flight: its first DEPTH tiles are
+  // requested now, and every processed tile is replaced by the one DEPTH
+  // steps ahead.
+  constexpr int DEPTH = (WAVES == 8) ? 1 : 2;
+  TileRegs buf[DEPTH];
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) {
+    const int tq = tile_begin + wave + d * WAVES;
+    if (tq < tile_end) load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
+  }
+
+  // --------------------------------------------------------------- prologue
+  if (t < kDim) {
     const int partner = half ? (t ^ 32) : (t ^ 1);
     const bool first = half ? (t < 32) : ((t & 1) == 0);
-    const int m = half ? (t & 31) : (t >> 1);
     const float qpv = __shfl(qv, partner, 64);
-    const float2 cs = reinterpret_cast<const float2*>(a.rope_cs + (int64_t)qp * 2 * kPairs)[m];
     sm.q[t] = first ? (qv * cs.x - qpv * cs.y) : (qpv * cs.y + qv * cs.x);
   }
-  __syncthreads();
-  float y = matvec_rows(pi_lh, sm.q, sm);
-  if (t < kDim) sm.qh[t] = y;
-  __syncthreads();
-  if (paper) {
-    if (t < kDim) sm.u[t] = sm.qh[t];
-  } else {
-    y = matvec_rows(a.qjl_s, sm.qh, sm);
-    if (t < kDim) sm.u[t] = y;
-  }
-  __syncthreads();
-  const float* lutk = a.lut_k + lh * 8;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int e = t + 256 * r;
-    const int d = e >> 4, nib = e & 15;
-    sm.ktab[e] = make_float2(sm.qh[d] * lutk[nib & 7], (nib & 8) ? sm.u[d] : -sm.u[d]);
+  for (int k = 0; k < COLS / 4; ++k) {
+    float* dst = sm.pi + ri * kPiPitch + cq * COLS + 4 * k;
+    dst[0] = pr[k].x; dst[1] = pr[k].y; dst[2] = pr[k].z; dst[3] = pr[k].w;
   }
-  if (t < 16) sm.vtab[t] = a.lut_v[lh * 8 + (t & 7)];
-  const float ebar_k = paper ? a.ebar[lh * 2 + 0] : 0.0f;
+  if (t < 16) sm.vtab[t] = cvv;
+  __syncthreads();
+  {
+    const float* x = sm.q + cq * COLS;
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < COLS / 4; ++k) {
+      acc = fmaf(pr[k].x, x[4 * k + 0], acc);
+      acc = fmaf(pr[k].y, x[4 * k + 1], acc);
+      acc = fmaf(pr[k].z, x[4 * k + 2], acc);
+      acc = fmaf(pr[k].w, x[4 * k + 3], acc);
+    }
+    sm.part[cq][ri] = acc;
+  }
+  __syncthreads();
+  if (t < kDim) {
+    float y = 0.0f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) y += sm.part[w][t];
+    sm.qh[t] = y;
+  }
+  __syncthreads();
+  if (!paper) {
+    const float* x = sm.qh + cq * COLS;
+    float acc = 0.0f;
+#pragma unroll
+    for (int k = 0; k < COLS / 4; ++k) {
+      acc = fmaf(sr[k].x, x[4 * k + 0], acc);
+      acc = fmaf(sr[k].y, x[4 * k + 1], acc);
+      acc = fmaf(sr[k].z, x[4 * k + 2], acc);
+      acc = fmaf(sr[k].w, x[4 * k + 3], acc);
+    }
+    sm.part[cq][ri] = acc;
+    __syncthreads();
+    if (t < kDim) {
+      float y = 0.0f;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) y += sm.part[w][t];
+      sm.u[t] = y;
+    }
+  } else {
+    if (t < kDim) sm.u[t] = sm.qh[t];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 1024 / NT; ++r) {
+    const int e = t + NT * r;
+    const int d = e >> 4, nib = e & 15;
+    const float cknib = __shfl(ck, nib & 7, 64);    // lane j of any wave holds c_K[j & 7]
+    sm.ktab[e] = make_float2(sm.qh[d] * cknib, (nib & 8) ? sm.u[d] : -sm.u[d]);
+  }
   __syncthreads();
 
-  // --------------------------------------------------------------- main loop
-  const uint8_t* kreg = a.k_codes + lh * a.slots * 32;
-  const uint8_t* vreg = a.v_codes + lh * a.slots * 32;
-  const uint2* sreg = reinterpret_cast<const uint2*>(a.scalars + lh * a.slots * 4);
-  const int64_t tile0 = s0 >> 6;
-
+  // -------------------------------------------------------------- main loop
   float m_run = -INFINITY;
   float l_lane = 0.0f;
-  float o0 = 0.0f, o1 = 0.0f, o2 = 0.0f, o3 = 0.0f;
   float sg = 0.0f;
+  float o0 = 0.0f, o1 = 0.0f, o2 = 0.0f, o3 = 0.0f;
+  const float lscale = a.logit_scale2;
+  const float2* ktab = sm.ktab;
+  const char* vtab = reinterpret_cast<const char*>(sm.vtab);
 
-  for (int tt = tile_begin + wave; tt < tile_end; tt += kWaves) {
-    const int64_t gt = tile0 + tt;
-    const uint4 kq0 = *reinterpret_cast<const uint4*>(kreg + tile_half_offset(gt, 0, lane));
-    const uint4 kq1 = *reinterpret_cast<const uint4*>(kreg + tile_half_offset(gt, 1, lane));
-    const uint4 vq0 = *reinterpret_cast<const uint4*>(vreg + tile_half_offset(gt, 0, lane));
-    const uint4 vq1 = *reinterpret_cast<const uint4*>(vreg + tile_half_offset(gt, 1, lane));
-    const int tok = tt * kTile + lane;
-    const bool tv = tok < n;
-    const uint2 sc = sreg[s0 + tok];
+  for (int tb = tile_begin + wave; tb < tile_end; tb += DEPTH * WAVES) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int tt = tb + d * WAVES;
+      if (tt >= tile_end) break;
+      const TileRegs& cur = buf[d];
+      const int tok = tt * kTile + lane;
+      const bool tv = tok < n;
 
-    // ---- key score, one lane per token
-    const uint32_t kw[8] = {kq0.x, kq0.y, kq0.z, kq0.w, kq1.x, kq1.y, kq1.z, kq1.w};
-    float A0 = 0.0f, A1 = 0.0f, B0 = 0.0f, B1 = 0.0f;
-#pragma unroll
-    for (int w8 = 0; w8 < 8; ++w8) {
-      const uint32_t x = kw[w8];
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj) {
-        const float2 e = sm.ktab[(w8 * 8 + jj) * 16 + ((x >> (4 * jj)) & 15u)];
-        if (jj & 1) { A1 += e.x; B1 += e.y; } else { A0 += e.x; B0 += e.y; }
+      // ---- key score, one lane per token. Two words (16 table reads) in
+      // flight at a time: the empty asm pins the partial sums so the compiler
+      // does not hoist every table read of the tile (registers, occupancy).
+      float A = 0.0f, B = 0.0f;
+      score_word(ktab + 0 * 128, cur.k0.x, A, B);
+      score_word(ktab + 1 * 128, cur.k0.y, A, B);
+      asm volatile("" : "+v"(A), "+v"(B));
+      score_word(ktab + 2 * 128, cur.k0.z, A, B);
+      score_word(ktab + 3 * 128, cur.k0.w, A, B);
+      asm volatile("" : "+v"(A), "+v"(B));
+      score_word(ktab + 4 * 128, cur.k1.x, A, B);
+      score_word(ktab + 5 * 128, cur.k1.y, A, B);
+      asm volatile("" : "+v"(A), "+v"(B));
+      score_word(ktab + 6 * 128, cur.k1.z, A, B);
+      score_word(ktab + 7 * 128, cur.k1.w, A, B);
+      const float nk = half_bits_to_float(cur.sc.x), gk = half_bits_to_float(cur.sc.x >> 16);
+      const float nv = half_bits_to_float(cur.sc.y), gv = half_bits_to_float(cur.sc.y >> 16);
+      const float coef = paper ? ebar_k : kQjlAlpha * gk;
+      float lg = nk * lscale * fmaf(coef, B, A);
+      lg = tv ? lg : -INFINITY;
+
+      // ---- online softmax (base 2), lazily rescaled
+      const float tmax = wave_max_uniform(lg);
+      if (tmax > m_run + kLazyRescale) {
+        const float f = __builtin_amdgcn_exp2f(m_run - tmax);
+        l_lane *= f;
+        sg *= f;
+        o0 *= f; o1 *= f; o2 *= f; o3 *= f;
+        m_run = tmax;
       }
-    }
-    const float nk = half_bits_to_float(sc.x), gk = half_bits_to_float(sc.x >> 16);
-    const float nv = half_bits_to_float(sc.y), gv = half_bits_to_float(sc.y >> 16);
-    const float coef = paper ? ebar_k : kQjlAlpha * gk;
-    float lg = nk * a.logit_scale2 * ((A0 + A1) + coef * (B0 + B1));
-    lg = tv ? lg : -INFINITY;
+      const float p = __builtin_amdgcn_exp2f(lg - m_run);
+      l_lane += p;
+      const float wv = tv ? p * nv * 0.125f : 0.0f;
+      sm.wp[wave][lane] = wv;
+      if (VQJL) sm.wg[wave][lane] = paper ? wv : wv * gv;
+      wave_lds_sync();
 
-    // ---- online softmax (base 2), lazily rescaled
-    const float tmax = wave_max(lg);
-    if (tmax > m_run + kLazyRescale) {
-      const float f = exp2f(m_run - tmax);
-      l_lane *= f;
-      o0 *= f; o1 *= f; o2 *= f; o3 *= f;
-      sg *= f;
-      m_run = tmax;
-    }
-    const float p = exp2f(lg - m_run);
-    l_lane += p;
-    const float wv = tv ? p * nv * 0.125f : 0.0f;
-    sm.wp[wave][lane] = wv;
-    if (VQJL) sm.wg[wave][lane] = paper ? wv : wv * gv;
-    wave_lds_sync();
-
-    // ---- value accumulate, one lane per dimension
-    const uint32_t vw[8] = {vq0.x, vq0.y, vq0.z, vq0.w, vq1.x, vq1.y, vq1.z, vq1.w};
-    const float4* wp4 = reinterpret_cast<const float4*>(sm.wp[wave]);
-    const float4* wg4 = reinterpret_cast<const float4*>(sm.wg[wave]);
-#pragma unroll
-    for (int w8 = 0; w8 < 8; ++w8) {
-      const uint32_t x = vw[w8];
-      const float4 wa = wp4[2 * w8], wb = wp4[2 * w8 + 1];
-      const float wt[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
-      o0 = fmaf(wt[0], sm.vtab[(x >> 0) & 7u], o0);
-      o1 = fmaf(wt[1], sm.vtab[(x >> 4) & 7u], o1);
-      o2 = fmaf(wt[2], sm.vtab[(x >> 8) & 7u], o2);
-      o3 = fmaf(wt[3], sm.vtab[(x >> 12) & 7u], o3);
-      o0 = fmaf(wt[4], sm.vtab[(x >> 16) & 7u], o0);
-      o1 = fmaf(wt[5], sm.vtab[(x >> 20) & 7u], o1);
-      o2 = fmaf(wt[6], sm.vtab[(x >> 24) & 7u], o2);
-      o3 = fmaf(wt[7], sm.vtab[(x >> 28) & 7u], o3);
+      // ---- value accumulate, one lane per dimension
+      const uint32_t vw[8] = {cur.v0.x, cur.v0.y, cur.v0.z, cur.v0.w, cur.v1.x, cur.v1.y, cur.v1.z, cur.v1.w};
+      const float4* wp4 = reinterpret_cast<const float4*>(sm.wp[wave]);
+  #pragma unroll
+      for (int w8 = 0; w8 < 8; ++w8) {
+        const uint32_t x = vw[w8];
+        const float4 wa = wp4[2 * w8], wb = wp4[2 * w8 + 1];
+        uint32_t off[8];
+        nibble_offsets4(x, off);     // (nibble & 7) * 4: float entries
+        o0 = fmaf(wa.x, *reinterpret_cast<const float*>(vtab + off[0]), o0);
+        o1 = fmaf(wa.y, *reinterpret_cast<const float*>(vtab + off[1]), o1);
+        o2 = fmaf(wa.z, *reinterpret_cast<const float*>(vtab + off[2]), o2);
+        o3 = fmaf(wa.w, *reinterpret_cast<const float*>(vtab + off[3]), o3);
+        o0 = fmaf(wb.x, *reinterpret_cast<const float*>(vtab + off[4]), o0);
+        o1 = fmaf(wb.y, *reinterpret_cast<const float*>(vtab + off[5]), o1);
+        o2 = fmaf(wb.z, *reinterpret_cast<const float*>(vtab + off[6]), o2);
+        o3 = fmaf(wb.w, *reinterpret_cast<const float*>(vtab + off[7]), o3);
+        if (w8 & 1) asm volatile("" : "+v"(o0), "+v"(o1), "+v"(o2), "+v"(o3));
+      }
       if (VQJL) {
-        const float4 ga = wg4[2 * w8], gb = wg4[2 * w8 + 1];
-        const float gt8[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) sg += ((x >> (4 * jj + 3)) & 1u) ? gt8[jj] : -gt8[jj];
+        const float4* wg4 = reinterpret_cast<const float4*>(sm.wg[wave]);
+  #pragma unroll
+        for (int w8 = 0; w8 < 8; ++w8) {
+          const uint32_t x = vw[w8];
+          const float4 ga = wg4[2 * w8], gb = wg4[2 * w8 + 1];
+          const float gt8[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
+  #pragma unroll
+          for (int jj = 0; jj < 8; ++jj) sg += ((x >> (4 * jj + 3)) & 1u) ? gt8[jj] : -gt8[jj];
+        }
       }
+      wave_lds_sync();   // wp/wg are rewritten by the next tile
+      const int tn = tt + DEPTH * WAVES;
+      if (tn < tile_end) load_tile(buf[d], kreg, vreg, sreg, tile0 + tn, s0, tn, lane);
     }
-    wave_lds_sync();   // wp/wg are rewritten by the next tile
   }
 
-  // ------------------------------------------------------- merge the 4 waves
-  const float l_wave = wave_sum(l_lane);
+  // ------------------------------------------------------ merge the waves
+  const float ov = (o0 + o1) + (o2 + o3);
+  const float l_wave = wave_sum_uniform(l_lane);
   if (lane == 0) { sm.wm[wave] = m_run; sm.wl[wave] = l_wave; }
-  sm.wo[wave][lane] = (o0 + o1) + (o2 + o3);
+  sm.wo[wave][lane] = ov;
   if (VQJL) sm.wsg[wave][lane] = sg;
   __syncthreads();
   float M = -INFINITY, L = 0.0f, O = 0.0f, SG = 0.0f;
   if (t < kDim) {
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) M = fmaxf(M, sm.wm[w]);
+    for (int w = 0; w < WAVES; ++w) M = fmaxf(M, sm.wm[w]);
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      const float f = exp2f(sm.wm[w] - M);
+    for (int w = 0; w < WAVES; ++w) {
+      const float f = __builtin_amdgcn_exp2f(sm.wm[w] - M);
       L += sm.wl[w] * f;
       O += sm.wo[w][t] * f;
       if (VQJL) SG += sm.wsg[w][t] * f;
@@ -275,7 +428,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a, int64_t total
     // until they are performed before counting the split in; the last split
     // reads the partials back with agent-scope loads. No block writes back or
     // invalidates the L2 (which a device-wide fence would do on every block).
-    float* part = a.partials + (unit * a.nsplit + split) * kPartialFloats;
+    float* part = a.partials + ((int64_t)unit * a.nsplit + split) * kPartialFloats;
     if (t < kDim) {
       __hip_atomic_store(part + 4 + t, O, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (VQJL) __hip_atomic_store(part + 4 + kDim + t, SG, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -294,14 +447,14 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a, int64_t total
     __syncthreads();
     if (!sm.last) return;
     if (t < kDim) {
-      float* base = a.partials + unit * a.nsplit * kPartialFloats;
+      float* base = a.partials + (int64_t)unit * a.nsplit * kPartialFloats;
       M = -INFINITY;
       for (int s = 0; s < participants; ++s)
         M = fmaxf(M, __hip_atomic_load(base + s * kPartialFloats, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
       L = 0.0f; O = 0.0f; SG = 0.0f;
       for (int s = 0; s < participants; ++s) {
         float* ps = base + s * kPartialFloats;
-        const float f = exp2f(__hip_atomic_load(ps, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - M);
+        const float f = __builtin_amdgcn_exp2f(__hip_atomic_load(ps, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - M);
         L += __hip_atomic_load(ps + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
         O += __hip_atomic_load(ps + 4 + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
         if (VQJL) SG += __hip_atomic_load(ps + 4 + kDim + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
@@ -311,7 +464,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a, int64_t total
     if (t == 0) __hip_atomic_store(a.counters + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
-  // ---------------------------------------------------------------- epilogue
+  // --------------------------------------------------------------- epilogue
   const float invL = 1.0f / L;
   if (t < kDim) { sm.oh[t] = O * invL; sm.sh[t] = SG * invL; }
   __syncthreads();
@@ -320,41 +473,90 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a, int64_t total
       const float ebar_v = a.ebar[lh * 2 + 1];
       if (t < kDim) sm.oh[t] += ebar_v * sm.sh[t];
     } else {
-      y = matvec_cols(a.qjl_s, sm.sh, sm);
-      if (t < kDim) sm.oh[t] += kQjlAlpha * y;
+      // o^ += alpha S^T s; thread (k, group) sums COLS rows of column k of S
+      const int k = t & 63;
+      float acc = 0.0f;
+#pragma unroll
+      for (int ii = 0; ii < COLS; ++ii) {
+        const int i = cq * COLS + ii;
+        acc = fmaf(a.qjl_s[i * kDim + k], sm.sh[i], acc);
+      }
+      sm.part[cq][k] = acc;
+      __syncthreads();
+      if (t < kDim) {
+        float y = 0.0f;
+#pragma unroll
+        for (int w = 0; w < WAVES; ++w) y += sm.part[w][t];
+        sm.oh[t] += kQjlAlpha * y;
+      }
     }
     __syncthreads();
   }
   if (a.flags & kVRotate) {
-    y = matvec_cols(pi_lh, sm.oh, sm);
-    if (t < kDim) store_out(a, unit, t, y);
+    // out_k = sum_i Pi[i][k] o^_i: thread (k, group) sums COLS rows
+    const int k = t & 63;
+    float acc = 0.0f;
+#pragma unroll
+    for (int ii = 0; ii < COLS; ++ii) {
+      const int i = cq * COLS + ii;
+      acc = fmaf(sm.pi[i * kPiPitch + k], sm.oh[i], acc);
+    }
+    sm.part[cq][k] = acc;
+    __syncthreads();
+    if (t < kDim) {
+      float y = 0.0f;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) y += sm.part[w][t];
+      store_out(a, unit, t, y);
+    }
   } else {
     if (t < kDim) store_out(a, unit, t, sm.oh[t]);
   }
 }
 
-void decode_plan(int units, int max_len, int* nsplit, int* split_tiles) {
+void decode_plan(int units, int max_len, int* waves, int* nsplit, int* split_tiles) {
   const int ntiles = max_len > 0 ? (max_len + 63) / 64 : 1;
-  const int target_blocks = 2048;
-  int ns = (target_blocks + units - 1) / units;
-  const int max_ns = (ntiles + kWaves - 1) / kWaves;   // at least one tile per wave
-  if (ns > max_ns) ns = max_ns;
-  if (ns < 1) ns = 1;
-  int st = (ntiles + ns - 1) / ns;
-  ns = (ntiles + st - 1) / st;
-  *nsplit = ns;
+  int w = ntiles >= 12 ? 8 : 4;
+  const char* ew = getenv("TQ_DECODE_WAVES");
+  if (ew && (atoi(ew) == 4 || atoi(ew) == 8)) w = atoi(ew);
+  int st;
+  const char* env = getenv("TQ_DECODE_SPLIT_TILES");
+  if (env && atoi(env) > 0) {
+    st = atoi(env);
+  } else {
+    // One block per unit when there are enough units to occupy every CU
+    // (a cross-block merge costs more than it balances); otherwise split the
+    // tiles so that each wave still gets at least one tile.
+    const int target_blocks = 256;
+    int ns = (target_blocks + units - 1) / units;
+    const int max_ns = (ntiles + w - 1) / w;
+    if (ns > max_ns) ns = max_ns;
+    if (ns < 1) ns = 1;
+    st = (ntiles + ns - 1) / ns;
+  }
+  if (st > ntiles) st = ntiles;
+  *waves = w;
   *split_tiles = st;
+  *nsplit = (ntiles + st - 1) / st;
 }
 
-hipError_t launch_decode(const DecodeArgs& a, hipStream_t st) {
+hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st) {
   const int64_t units = (int64_t)a.nlayers * a.B * a.H;
   const int64_t total = units * a.nsplit;
   const int64_t per_xcd = (total + kXcds - 1) / kXcds;
   const int64_t blocks = per_xcd * kXcds;
-  if (a.flags & kVQjl)
-    hipLaunchKernelGGL(decode_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, st, a, total, per_xcd);
-  else
-    hipLaunchKernelGGL(decode_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, st, a, total, per_xcd);
+  const bool vq = (a.flags & kVQjl) != 0;
+  if (waves == 8) {
+    if (vq)
+      hipLaunchKernelGGL((decode_kernel<8, true>), dim3((unsigned)blocks), dim3(512), 0, st, a, (int)total, (int)per_xcd);
+    else
+      hipLaunchKernelGGL((decode_kernel<8, false>), dim3((unsigned)blocks), dim3(512), 0, st, a, (int)total, (int)per_xcd);
+  } else {
+    if (vq)
+      hipLaunchKernelGGL((decode_kernel<4, true>), dim3((unsigned)blocks), dim3(256), 0, st, a, (int)total, (int)per_xcd);
+    else
+      hipLaunchKernelGGL((decode_kernel<4, false>), dim3((unsigned)blocks), dim3(256), 0, st, a, (int)total, (int)per_xcd);
+  }
   return hipGetLastError();
 }
 

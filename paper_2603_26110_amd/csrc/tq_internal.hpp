@@ -62,8 +62,8 @@ constexpr int kPartialFloats = 2 * 64 + 4;   // m, l, pad, pad, o[64], s[64]
 // Launchers (return the HIP status of the launch).
 hipError_t launch_rope_table(float* cs, int positions, double base, hipStream_t st);
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t st);
-void decode_plan(int units, int max_len, int* nsplit, int* split_tiles);
-hipError_t launch_decode(const DecodeArgs& a, hipStream_t st);
+void decode_plan(int units, int max_len, int* waves, int* nsplit, int* split_tiles);
+hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st);
 hipError_t launch_calibrate(const float* x, int nheads, int ncal, float* pi_out,
                             float* sing_out, hipStream_t st);
 

@@ -6,8 +6,9 @@
 //   quantize_tiles_kernel   one lane per token, 64 tokens per wave, for
 //                           prefill-sized T. Pi and S sit in LDS and are read
 //                           as wave-wide broadcasts.
-//   quantize_vectors_kernel one wave per token-head (one lane per dimension),
-//                           for decode-step appends with small T.
+//   quantize_vectors_kernel one wave per vector (one lane per dimension; the
+//                           key and the value of a token-head in parallel), for
+//                           decode-step appends with small T.
 // Both evaluate the rotation as an fma chain over k ascending and the
 // quantizer steps with the fixed binary32 order of quantize_lane, so a token
 // gets the same codes from either kernel.
@@ -209,8 +210,12 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
   }
 }
 
-// ----------------------------------------------- wave-per-token-head kernel
-// Block: 4 waves, each one (layer, sequence, token, head); lane = dimension.
+// ----------------------------------------------- wave-per-vector kernel
+// Block: 2 waves for one (layer, sequence, token, head): wave 0 quantizes the
+// key, wave 1 the value; lane = dimension. Everything a wave needs (its input
+// element, row i of Pi and of S, the table) is requested up front, so a
+// decode-step append costs about one memory round trip plus the fixed-order
+// arithmetic chains.
 struct WaveScratch {
   float x[kDim];
   float r[kDim];
@@ -222,11 +227,26 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Row i of a 64 x 64 matrix times the vector staged in `v` (LDS): fma chain
+// over k ascending, the order of rotate_lane and quantize_lane.
+__device__ __forceinline__ float row_dot(const float4 (&row)[16], const float* v) {
+  float acc = 0.0f;
+#pragma unroll
+  for (int k4 = 0; k4 < 16; ++k4) {
+    acc = fmaf(row[k4].x, v[4 * k4 + 0], acc);
+    acc = fmaf(row[k4].y, v[4 * k4 + 1], acc);
+    acc = fmaf(row[k4].z, v[4 * k4 + 2], acc);
+    acc = fmaf(row[k4].w, v[4 * k4 + 3], acc);
+  }
+  return acc;
+}
+
 // Quantize the vector whose element i lane i holds in `xh`; same arithmetic
 // order as quantize_lane. Returns the lane's nibble; n16/g16 are uniform.
 __device__ __forceinline__ uint32_t quantize_wave(float xh, const float (&c)[8], const float (&t)[7],
-                                                  const float* S, int sign_mode, WaveScratch* ws,
-                                                  int i, uint32_t* n16, uint32_t* g16) {
+                                                  const float4 (&srow)[16], int sign_mode,
+                                                  WaveScratch* ws, int i, uint32_t* n16,
+                                                  uint32_t* g16) {
   ws->x[i] = xh;
   wave_sync_lds();
   float s = 0.0f;
@@ -252,17 +272,7 @@ __device__ __forceinline__ uint32_t quantize_wave(float xh, const float (&c)[8],
   const float g = sqrtf(gs);
   uint32_t bit = 0;
   if (sign_mode == 1) {
-    const float4* row = reinterpret_cast<const float4*>(S + i * kDim);
-    float acc = 0.0f;
-#pragma unroll
-    for (int k4 = 0; k4 < kDim / 4; ++k4) {
-      const float4 sv = row[k4];
-      acc = fmaf(sv.x, ws->r[4 * k4 + 0], acc);
-      acc = fmaf(sv.y, ws->r[4 * k4 + 1], acc);
-      acc = fmaf(sv.z, ws->r[4 * k4 + 2], acc);
-      acc = fmaf(sv.w, ws->r[4 * k4 + 3], acc);
-    }
-    bit = (acc < 0.0f) ? 0u : 1u;
+    bit = (row_dot(srow, ws->r) < 0.0f) ? 0u : 1u;
   } else if (sign_mode == 2) {
     bit = (r < 0.0f) ? 0u : 1u;
   }
@@ -271,31 +281,13 @@ __device__ __forceinline__ uint32_t quantize_wave(float xh, const float (&c)[8],
   return idx | (bit << 3);
 }
 
-// Pi row i times the vector held across lanes (staged in ws->x): fma chain
-// over k ascending, the same order as rotate_lane.
-__device__ __forceinline__ float rotate_wave(float xi, const float* pi_lh, WaveScratch* ws, int i) {
-  ws->x[i] = xi;
-  wave_sync_lds();
-  const float4* row = reinterpret_cast<const float4*>(pi_lh + i * kDim);
-  float acc = 0.0f;
-#pragma unroll
-  for (int k4 = 0; k4 < kDim / 4; ++k4) {
-    const float4 p = row[k4];
-    acc = fmaf(p.x, ws->x[4 * k4 + 0], acc);
-    acc = fmaf(p.y, ws->x[4 * k4 + 1], acc);
-    acc = fmaf(p.z, ws->x[4 * k4 + 2], acc);
-    acc = fmaf(p.w, ws->x[4 * k4 + 3], acc);
-  }
-  wave_sync_lds();   // ws->x is reused by the caller
-  return acc;
-}
-
 template <bool F16>
-__global__ __launch_bounds__(256) void quantize_vectors_kernel(QuantArgs a, int64_t total) {
-  __shared__ WaveScratch scratch[4];
+__global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, int64_t total) {
+  __shared__ WaveScratch scratch[2];
   const int wave = threadIdx.x >> 6, i = threadIdx.x & 63;
-  const int64_t th = (int64_t)blockIdx.x * 4 + wave;
+  const int64_t th = blockIdx.x;
   if (th >= total) return;
+  const bool is_v = wave == 1;
   WaveScratch* ws = &scratch[wave];
   const int h = (int)(th % a.H);
   int64_t rest = th / a.H;
@@ -312,55 +304,70 @@ __global__ __launch_bounds__(256) void quantize_vectors_kernel(QuantArgs a, int6
   if (!rotated && (pos < 0 || pos >= a.rope_positions)) return;
   const bool paper = (a.flags & kQjlPaper) != 0;
   const int ksign = paper ? 2 : 1;
-  const int vsign = (a.flags & kVQjl) ? ksign : 0;
-  const float* pi_lh = a.pi + lh * kDim * kDim;
+  const int sign_mode = is_v ? ((a.flags & kVQjl) ? ksign : 0) : ksign;
+  const bool rotate = !rotated && (!is_v || (a.flags & kVRotate));
   const int64_t row = ((((int64_t)li * a.B + b) * a.T + j) * a.H + h) * kDim;
-  const int64_t tile = slot >> 6;
-  const int r = (int)(slot & 63);
 
-  float ck[8], tk[7], cv[8], tv[7];
-  load_table(a.lut_k + lh * 8, ck, tk);
-  load_table(a.lut_v + lh * 8, cv, tv);
+  // ---- loads, all issued before any arithmetic
+  float x = load_in(is_v ? a.v : a.k, row + i, F16);
+  float4 prow[16], srow[16];
+  if (rotate) {
+    const float4* p = reinterpret_cast<const float4*>(a.pi + lh * kDim * kDim + i * kDim);
+#pragma unroll
+    for (int k4 = 0; k4 < 16; ++k4) prow[k4] = p[k4];
+  }
+  if (sign_mode == 1) {
+    const float4* p = reinterpret_cast<const float4*>(a.qjl_s + i * kDim);
+#pragma unroll
+    for (int k4 = 0; k4 < 16; ++k4) srow[k4] = p[k4];
+  }
+  float c[8], t[7];
+  load_table((is_v ? a.lut_v : a.lut_k) + lh * 8, c, t);
+  const bool half = (a.flags & kRopeHalf) != 0;
+  float2 cs = make_float2(1.0f, 0.0f);
+  if (!is_v && !rotated) {
+    const int m = half ? (i & 31) : (i >> 1);
+    cs = reinterpret_cast<const float2*>(a.rope_cs + (int64_t)pos * 2 * kPairs)[m];
+  }
 
-  // ---- K
-  float x = load_in(a.k, row + i, F16);
-  if (!rotated) {
-    const bool half = (a.flags & kRopeHalf) != 0;
+  // ---- RoPE (keys) and rotation
+  if (!is_v && !rotated) {
     const int partner = half ? (i ^ 32) : (i ^ 1);
     const bool first = half ? (i < 32) : ((i & 1) == 0);
-    const int m = half ? (i & 31) : (i >> 1);
     const float xp = __shfl(x, partner, 64);
-    const float2 cs = reinterpret_cast<const float2*>(a.rope_cs + (int64_t)pos * 2 * kPairs)[m];
     // pair (a, b): x'_a = x_a c - x_b s, x'_b = x_a s + x_b c
     x = first ? (x * cs.x - xp * cs.y) : (xp * cs.y + x * cs.x);
-    x = rotate_wave(x, pi_lh, ws, i);
   }
-  uint32_t nk, gk;
-  const uint32_t knib = quantize_wave(x, ck, tk, a.qjl_s, ksign, ws, i, &nk, &gk);
-  // gather 8 nibbles per 32-bit word: lane 8w ends with word w
-  uint32_t word = knib << (4 * (i & 7));
-  word |= __shfl_xor(word, 1, 64);
-  word |= __shfl_xor(word, 2, 64);
-  word |= __shfl_xor(word, 4, 64);
-  uint8_t* kreg = a.k_codes + lh * a.slots * 32;
-  if ((i & 7) == 0) {
-    const int w = i >> 3;
-    *reinterpret_cast<uint32_t*>(kreg + tile_half_offset(tile, w >> 2, r) + (w & 3) * 4) = word;
+  if (rotate) {
+    ws->x[i] = x;
+    wave_sync_lds();
+    x = row_dot(prow, ws->x);
+    wave_sync_lds();   // ws->x is rewritten by quantize_wave
   }
 
-  // ---- V
-  wave_sync_lds();
-  float xv = load_in(a.v, row + i, F16);
-  if (!rotated && (a.flags & kVRotate)) xv = rotate_wave(xv, pi_lh, ws, i);
-  uint32_t nv, gv;
-  const uint32_t vnib = quantize_wave(xv, cv, tv, a.qjl_s, vsign, ws, i, &nv, &gv);
-  uint8_t* vreg = a.v_codes + lh * a.slots * 32;
-  const int c = r >> 5, G4 = (r & 31) >> 3, jj = r & 7;
-  uint32_t* addr = reinterpret_cast<uint32_t*>(vreg + tile_half_offset(tile, c, i) + G4 * 4);
-  store_v_word(addr, vnib << (4 * jj), 15u << (4 * jj));
-  if (i == 0) {
-    *reinterpret_cast<uint2*>(a.scalars + (lh * a.slots + slot) * 4) =
-        make_uint2(nk | (gk << 16), nv | (gv << 16));
+  uint32_t n16, g16;
+  const uint32_t nib = quantize_wave(x, c, t, srow, sign_mode, ws, i, &n16, &g16);
+  const int64_t tile = slot >> 6;
+  const int r = (int)(slot & 63);
+  if (!is_v) {
+    // key: token-major, 8 nibbles per 32-bit word; lane 8w ends with word w
+    uint32_t word = nib << (4 * (i & 7));
+    word |= __shfl_xor(word, 1, 64);
+    word |= __shfl_xor(word, 2, 64);
+    word |= __shfl_xor(word, 4, 64);
+    uint8_t* kreg = a.k_codes + lh * a.slots * 32;
+    if ((i & 7) == 0) {
+      const int w = i >> 3;
+      *reinterpret_cast<uint32_t*>(kreg + tile_half_offset(tile, w >> 2, r) + (w & 3) * 4) = word;
+    }
+    if (i == 0) reinterpret_cast<uint32_t*>(a.scalars + (lh * a.slots + slot) * 4)[0] = n16 | (g16 << 16);
+  } else {
+    // value: dimension-major, one nibble of dimension i's word for this slot
+    uint8_t* vreg = a.v_codes + lh * a.slots * 32;
+    const int cc = r >> 5, G4 = (r & 31) >> 3, jj = r & 7;
+    uint32_t* addr = reinterpret_cast<uint32_t*>(vreg + tile_half_offset(tile, cc, i) + G4 * 4);
+    store_v_word(addr, nib << (4 * jj), 15u << (4 * jj));
+    if (i == 0) reinterpret_cast<uint32_t*>(a.scalars + (lh * a.slots + slot) * 4)[1] = n16 | (g16 << 16);
   }
 }
 
@@ -375,11 +382,10 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t st) {
       hipLaunchKernelGGL(quantize_tiles_kernel<false>, grid, dim3(128), lds, st, a);
   } else {
     const int64_t total = (int64_t)a.nlayers * a.B * a.T * a.H;
-    const int64_t blocks = (total + 3) / 4;
     if (f16)
-      hipLaunchKernelGGL(quantize_vectors_kernel<true>, dim3((unsigned)blocks), dim3(256), 0, st, a, total);
+      hipLaunchKernelGGL(quantize_vectors_kernel<true>, dim3((unsigned)total), dim3(128), 0, st, a, total);
     else
-      hipLaunchKernelGGL(quantize_vectors_kernel<false>, dim3((unsigned)blocks), dim3(256), 0, st, a, total);
+      hipLaunchKernelGGL(quantize_vectors_kernel<false>, dim3((unsigned)total), dim3(128), 0, st, a, total);
   }
   return hipGetLastError();
 }

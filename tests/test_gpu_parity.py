@@ -31,14 +31,16 @@ def test_library_loaded_and_version():
 
 def test_rope_table_matches_oracle():
     # fp64 cos/sin on the GPU and in libm may differ in the last fp64 bits;
-    # after rounding to fp32 the tables agree to within one fp32 ulp.
+    # after rounding to fp32 the tables agree to one fp32 ulp, except next to
+    # zeros of sin/cos, where the absolute difference stays at fp64 noise.
     cs = tq.rope_table(8256).cpu().numpy()
     ref = oracle.rope_table(8256)
     ia = cs.view(np.int32).astype(np.int64)
     ib = ref.view(np.int32).astype(np.int64)
     same_sign = np.sign(cs) == np.sign(ref)
     ulps = np.where(same_sign, np.abs(ia - ib), np.abs(ia) + np.abs(ib))
-    assert np.max(ulps) <= 1
+    absdiff = np.abs(cs.astype(np.float64) - ref.astype(np.float64))
+    assert np.all((ulps <= 1) | (absdiff <= 1e-10))
     assert np.mean(cs == ref) > 0.999
 
 
