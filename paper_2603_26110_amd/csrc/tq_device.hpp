@@ -60,17 +60,66 @@ __device__ __forceinline__ int64_t tile_half_offset(int64_t tile, int c, int r) 
 // the projected sign of row i is an fma chain over k ascending, so any kernel
 // that calls this on the same x^ produces the same bits.
 //   xh[64]   rotated vector (overwritten by the residual r)
-//   c[8]     ascending table, t[7] its midpoints (0.5f * (c_m + c_{m+1}))
+//   L        ascending table and its midpoints (0.5f * (c_m + c_{m+1}))
 //   S        64 x 64 projection in LDS (row-major); unused unless sign_mode == 1
 //   sign_mode 0 none, 1 projected (S r), 2 per element (r)
 //   words[8] out: nibble words (idx | sign << 3)
+// The eight levels and seven midpoints of one table as named register values.
+// Named members (no arrays) keep the level choice a chain of selects between
+// registers; an array indexed inside a loop gets folded into an indexed load
+// from private memory, which the compiler then spills to LDS or scratch.
+struct Levels {
+  float c0, c1, c2, c3, c4, c5, c6, c7;
+  float t0, t1, t2, t3, t4, t5, t6;
+};
+
+__device__ __forceinline__ Levels load_levels(const float* lut) {
+  Levels L;
+  L.c0 = lut[0]; L.c1 = lut[1]; L.c2 = lut[2]; L.c3 = lut[3];
+  L.c4 = lut[4]; L.c5 = lut[5]; L.c6 = lut[6]; L.c7 = lut[7];
+  L.t0 = 0.5f * (L.c0 + L.c1); L.t1 = 0.5f * (L.c1 + L.c2); L.t2 = 0.5f * (L.c2 + L.c3);
+  L.t3 = 0.5f * (L.c3 + L.c4); L.t4 = 0.5f * (L.c4 + L.c5); L.t5 = 0.5f * (L.c5 + L.c6);
+  L.t6 = 0.5f * (L.c6 + L.c7);
+  return L;
+}
+
+// Nearest level of u by the midpoints (ties go to the lower level): returns
+// the level, its index in *idx.
+// The levels are passed as separate values, which callers pin in registers
+// once (TQ_PIN_LEVELS): the selects then pick between register values, where a
+// select between two loads of a table would become one load at a computed
+// offset, from private memory.
+#define TQ_PIN_LEVELS(L)                                                                  \
+  float L##_0 = L.c0, L##_1 = L.c1, L##_2 = L.c2, L##_3 = L.c3, L##_4 = L.c4, L##_5 = L.c5, \
+        L##_6 = L.c6, L##_7 = L.c7;                                                       \
+  asm volatile("" : "+v"(L##_0), "+v"(L##_1), "+v"(L##_2), "+v"(L##_3), "+v"(L##_4),     \
+               "+v"(L##_5), "+v"(L##_6), "+v"(L##_7))
+#define TQ_LEVELS(L) L, L##_0, L##_1, L##_2, L##_3, L##_4, L##_5, L##_6, L##_7
+
+__device__ __forceinline__ float nearest_level(float u, const Levels& L, float c0, float c1,
+                                               float c2, float c3, float c4, float c5, float c6,
+                                               float c7, uint32_t* idx) {
+  uint32_t i = 0;
+  float lv = c0;
+  bool a;
+  a = u > L.t0; i += a ? 1u : 0u; lv = a ? c1 : lv;
+  a = u > L.t1; i += a ? 1u : 0u; lv = a ? c2 : lv;
+  a = u > L.t2; i += a ? 1u : 0u; lv = a ? c3 : lv;
+  a = u > L.t3; i += a ? 1u : 0u; lv = a ? c4 : lv;
+  a = u > L.t4; i += a ? 1u : 0u; lv = a ? c5 : lv;
+  a = u > L.t5; i += a ? 1u : 0u; lv = a ? c6 : lv;
+  a = u > L.t6; i += a ? 1u : 0u; lv = a ? c7 : lv;
+  *idx = i;
+  return lv;
+}
+
 struct QuantOut {
   uint32_t n16, g16;
 };
 
-__device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const float (&c)[8],
-                                                  const float (&t)[7], const float* S,
-                                                  int sign_mode, uint32_t (&words)[8]) {
+__device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Levels& L,
+                                                  const float* S, int sign_mode,
+                                                  uint32_t (&words)[8]) {
   float s = 0.0f;
 #pragma unroll
   for (int i = 0; i < kDim; ++i) s = fmaf(xh[i], xh[i], s);
@@ -78,17 +127,12 @@ __device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const float
   const float inv = (n == 0.0f) ? 0.0f : 8.0f / n;
 #pragma unroll
   for (int w = 0; w < 8; ++w) words[w] = 0u;
+  TQ_PIN_LEVELS(L);
 #pragma unroll
   for (int i = 0; i < kDim; ++i) {
     const float u = xh[i] * inv;
-    uint32_t idx = 0;
-    float lv = c[0];
-#pragma unroll
-    for (int m = 0; m < 7; ++m) {
-      const bool above = u > t[m];
-      idx += above ? 1u : 0u;
-      lv = above ? c[m + 1] : lv;
-    }
+    uint32_t idx;
+    const float lv = nearest_level(u, TQ_LEVELS(L), &idx);
     words[i >> 3] |= idx << (4 * (i & 7));
     xh[i] = u - lv;   // residual r_i
   }

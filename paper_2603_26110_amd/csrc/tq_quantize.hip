@@ -87,13 +87,6 @@ __device__ __forceinline__ void rotate_lane(float (&x)[kDim], const float* s_pi,
   for (int i = 0; i < kDim; ++i) x[i] = s_col[i * kDim + lane];
 }
 
-__device__ __forceinline__ void load_table(const float* lut, float (&c)[8], float (&t)[7]) {
-#pragma unroll
-  for (int m = 0; m < 8; ++m) c[m] = lut[m];
-#pragma unroll
-  for (int m = 0; m < 7; ++m) t[m] = 0.5f * (c[m] + c[m + 1]);
-}
-
 // Write one dimension-major V nibble group: `mask` selects the nibbles of
 // `word` this writer owns. Whole words are stored; partial words are merged
 // with atomics so concurrent writers of neighbouring slots do not collide.
@@ -130,9 +123,8 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
     s_pi[e] = a.pi[lh * kDim * kDim + e];
     s_S[e] = a.qjl_s[e];
   }
-  float ck[8], tk[7], cv[8], tv[7];
-  load_table(a.lut_k + lh * 8, ck, tk);
-  load_table(a.lut_v + lh * 8, cv, tv);
+  const Levels Lk = load_levels(a.lut_k + lh * 8);
+  const Levels Lv = load_levels(a.lut_v + lh * 8);
   __syncthreads();
 
   const int j0 = blockIdx.x * 128 + wave * kTile;
@@ -157,7 +149,7 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
     rotate_lane(x, s_pi, s_col, lane);
   }
   uint32_t kw[8];
-  const QuantOut qk = quantize_lane(x, ck, tk, s_S, ksign, kw);
+  const QuantOut qk = quantize_lane(x, Lk, s_S, ksign, kw);
   if (ok) {
     const int64_t tile = slot >> 6;
     const int r = (int)(slot & 63);
@@ -170,7 +162,7 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
   for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.v, row + i, F16) : 0.0f;
   if (!rotated && (a.flags & kVRotate)) rotate_lane(x, s_pi, s_col, lane);
   uint32_t vw[8];
-  const QuantOut qv = quantize_lane(x, cv, tv, s_S, vsign, vw);
+  const QuantOut qv = quantize_lane(x, Lv, s_S, vsign, vw);
   if (ok) {
     *reinterpret_cast<uint2*>(a.scalars + (lh * a.slots + slot) * 4) =
         make_uint2(qk.n16 | (qk.g16 << 16), qv.n16 | (qv.g16 << 16));
@@ -212,13 +204,17 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
 
 // ----------------------------------------------- wave-per-vector kernel
 // Block: 2 waves for one (layer, sequence, token, head): wave 0 quantizes the
-// key, wave 1 the value; lane = dimension. Everything a wave needs (its input
-// element, row i of Pi and of S, the table) is requested up front, so a
-// decode-step append costs about one memory round trip plus the fixed-order
-// arithmetic chains.
-struct WaveScratch {
-  float x[kDim];
-  float r[kDim];
+// key, wave 1 the value; lane = dimension. Pi and S are read with coalesced
+// 16-byte loads by the whole block and stored transposed in LDS (rows padded
+// to 65 floats), so that lane i walks column i of the transpose, i.e. row i of
+// the matrix, with conflict-free reads; the fma chains keep k ascending.
+constexpr int kTStride = kDim + 1;
+
+struct VectorSmem {
+  float piT[kDim * kTStride];   // piT[k * 65 + i] = Pi[i][k]
+  float sT[kDim * kTStride];    // sT[k * 65 + i] = S[i][k]
+  float x[2][kDim];
+  float r[2][kDim];
 };
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -227,52 +223,60 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Row i of a 64 x 64 matrix times the vector staged in `v` (LDS): fma chain
-// over k ascending, the order of rotate_lane and quantize_lane.
-__device__ __forceinline__ float row_dot(const float4 (&row)[16], const float* v) {
+// Row i of a 64 x 64 matrix (stored transposed in `mT`) times the vector
+// staged in `v`: fma chain over k ascending, the order of rotate_lane and
+// quantize_lane.
+__device__ __forceinline__ float row_dot_t(const float* mT, const float* v, int i) {
   float acc = 0.0f;
 #pragma unroll
-  for (int k4 = 0; k4 < 16; ++k4) {
-    acc = fmaf(row[k4].x, v[4 * k4 + 0], acc);
-    acc = fmaf(row[k4].y, v[4 * k4 + 1], acc);
-    acc = fmaf(row[k4].z, v[4 * k4 + 2], acc);
-    acc = fmaf(row[k4].w, v[4 * k4 + 3], acc);
+  for (int k4 = 0; k4 < kDim / 4; ++k4) {
+    const float4 vv = reinterpret_cast<const float4*>(v)[k4];
+    acc = fmaf(mT[(4 * k4 + 0) * kTStride + i], vv.x, acc);
+    acc = fmaf(mT[(4 * k4 + 1) * kTStride + i], vv.y, acc);
+    acc = fmaf(mT[(4 * k4 + 2) * kTStride + i], vv.z, acc);
+    acc = fmaf(mT[(4 * k4 + 3) * kTStride + i], vv.w, acc);
   }
   return acc;
 }
 
 // Quantize the vector whose element i lane i holds in `xh`; same arithmetic
 // order as quantize_lane. Returns the lane's nibble; n16/g16 are uniform.
-__device__ __forceinline__ uint32_t quantize_wave(float xh, const float (&c)[8], const float (&t)[7],
-                                                  const float4 (&srow)[16], int sign_mode,
-                                                  WaveScratch* ws, int i, uint32_t* n16,
-                                                  uint32_t* g16) {
-  ws->x[i] = xh;
+__device__ __forceinline__ uint32_t quantize_wave(float xh, const Levels& L,
+                                                  const float* sT, int sign_mode, float* xs,
+                                                  float* rs, int i, uint32_t* n16, uint32_t* g16) {
+  xs[i] = xh;
   wave_sync_lds();
   float s = 0.0f;
 #pragma unroll
-  for (int k = 0; k < kDim; ++k) s = fmaf(ws->x[k], ws->x[k], s);
+  for (int k4 = 0; k4 < kDim / 4; ++k4) {
+    const float4 v = reinterpret_cast<const float4*>(xs)[k4];
+    s = fmaf(v.x, v.x, s);
+    s = fmaf(v.y, v.y, s);
+    s = fmaf(v.z, v.z, s);
+    s = fmaf(v.w, v.w, s);
+  }
   const float n = sqrtf(s);
   const float inv = (n == 0.0f) ? 0.0f : 8.0f / n;
   const float u = xh * inv;
-  uint32_t idx = 0;
-  float lv = c[0];
-#pragma unroll
-  for (int m = 0; m < 7; ++m) {
-    const bool above = u > t[m];
-    idx += above ? 1u : 0u;
-    lv = above ? c[m + 1] : lv;
-  }
+  TQ_PIN_LEVELS(L);
+  uint32_t idx;
+  const float lv = nearest_level(u, TQ_LEVELS(L), &idx);
   const float r = u - lv;
-  ws->r[i] = r;
+  rs[i] = r;
   wave_sync_lds();
   float gs = 0.0f;
 #pragma unroll
-  for (int k = 0; k < kDim; ++k) gs = fmaf(ws->r[k], ws->r[k], gs);
+  for (int k4 = 0; k4 < kDim / 4; ++k4) {
+    const float4 v = reinterpret_cast<const float4*>(rs)[k4];
+    gs = fmaf(v.x, v.x, gs);
+    gs = fmaf(v.y, v.y, gs);
+    gs = fmaf(v.z, v.z, gs);
+    gs = fmaf(v.w, v.w, gs);
+  }
   const float g = sqrtf(gs);
   uint32_t bit = 0;
   if (sign_mode == 1) {
-    bit = (row_dot(srow, ws->r) < 0.0f) ? 0u : 1u;
+    bit = (row_dot_t(sT, rs, i) < 0.0f) ? 0u : 1u;
   } else if (sign_mode == 2) {
     bit = (r < 0.0f) ? 0u : 1u;
   }
@@ -281,54 +285,73 @@ __device__ __forceinline__ uint32_t quantize_wave(float xh, const float (&c)[8],
   return idx | (bit << 3);
 }
 
+// Coalesced copy of a 64 x 64 row-major matrix into its padded transpose, in
+// two steps so that the loads can be issued early: thread t holds float4
+// number t + 128 j (row e / 16, columns 4 (e % 16) .. 4 (e % 16) + 3).
+struct MatrixSlice {
+  float4 v[8];
+};
+
+__device__ __forceinline__ void load_slice(const float* __restrict__ m, MatrixSlice& sl, int t) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) sl.v[j] = reinterpret_cast<const float4*>(m)[t + 128 * j];
+}
+
+__device__ __forceinline__ void store_slice_transposed(const MatrixSlice& sl, float* mT, int t) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int e = t + 128 * j, row = e >> 4, col = (e & 15) * 4;
+    mT[(col + 0) * kTStride + row] = sl.v[j].x;
+    mT[(col + 1) * kTStride + row] = sl.v[j].y;
+    mT[(col + 2) * kTStride + row] = sl.v[j].z;
+    mT[(col + 3) * kTStride + row] = sl.v[j].w;
+  }
+}
+
 template <bool F16>
-__global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, int64_t total) {
-  __shared__ WaveScratch scratch[2];
+__global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, uint32_t total) {
+  __shared__ VectorSmem sm;
   const int wave = threadIdx.x >> 6, i = threadIdx.x & 63;
-  const int64_t th = blockIdx.x;
+  const uint32_t th = blockIdx.x;   // the host keeps the token-head count below 2^31
   if (th >= total) return;
   const bool is_v = wave == 1;
-  WaveScratch* ws = &scratch[wave];
-  const int h = (int)(th % a.H);
-  int64_t rest = th / a.H;
-  const int j = (int)(rest % a.T);
-  rest /= a.T;
-  const int b = (int)(rest % a.B);
-  const int li = (int)(rest / a.B);
-  const int l = a.layer0 + li;
+  const uint32_t h = th % (uint32_t)a.H;
+  uint32_t rest = th / (uint32_t)a.H;
+  const uint32_t j = rest % (uint32_t)a.T;
+  rest /= (uint32_t)a.T;
+  const uint32_t b = rest % (uint32_t)a.B;
+  const uint32_t li = rest / (uint32_t)a.B;
+  const int l = a.layer0 + (int)li;
   const int64_t lh = (int64_t)l * a.H + h;
   const bool rotated = (a.flags & kInputRotated) != 0;
-  const int64_t slot = a.slot0[b] + j;
-  const int pos = a.pos0[b] + j;
-  if (slot < 0 || slot >= a.slots) return;
-  if (!rotated && (pos < 0 || pos >= a.rope_positions)) return;
   const bool paper = (a.flags & kQjlPaper) != 0;
   const int ksign = paper ? 2 : 1;
   const int sign_mode = is_v ? ((a.flags & kVQjl) ? ksign : 0) : ksign;
+  const bool any_rotate = !rotated;                       // keys rotate unless pre-rotated
   const bool rotate = !rotated && (!is_v || (a.flags & kVRotate));
+  const bool any_proj = !paper;                           // keys use the projection unless paper
   const int64_t row = ((((int64_t)li * a.B + b) * a.T + j) * a.H + h) * kDim;
 
-  // ---- loads, all issued before any arithmetic
+  // ---- loads that do not depend on the slot, issued first
   float x = load_in(is_v ? a.v : a.k, row + i, F16);
-  float4 prow[16], srow[16];
-  if (rotate) {
-    const float4* p = reinterpret_cast<const float4*>(a.pi + lh * kDim * kDim + i * kDim);
-#pragma unroll
-    for (int k4 = 0; k4 < 16; ++k4) prow[k4] = p[k4];
-  }
-  if (sign_mode == 1) {
-    const float4* p = reinterpret_cast<const float4*>(a.qjl_s + i * kDim);
-#pragma unroll
-    for (int k4 = 0; k4 < 16; ++k4) srow[k4] = p[k4];
-  }
-  float c[8], t[7];
-  load_table((is_v ? a.lut_v : a.lut_k) + lh * 8, c, t);
+  const Levels L = load_levels((is_v ? a.lut_v : a.lut_k) + lh * 8);
+  MatrixSlice pi_sl, s_sl;
+  if (any_rotate) load_slice(a.pi + lh * kDim * kDim, pi_sl, threadIdx.x);
+  if (any_proj) load_slice(a.qjl_s, s_sl, threadIdx.x);
+  const int64_t slot = a.slot0[b] + j;
+  const int pos = a.pos0[b] + (int)j;
+  // block-uniform exits (before any barrier)
+  if (slot < 0 || slot >= a.slots) return;
+  if (!rotated && (pos < 0 || pos >= a.rope_positions)) return;
   const bool half = (a.flags & kRopeHalf) != 0;
   float2 cs = make_float2(1.0f, 0.0f);
   if (!is_v && !rotated) {
     const int m = half ? (i & 31) : (i >> 1);
     cs = reinterpret_cast<const float2*>(a.rope_cs + (int64_t)pos * 2 * kPairs)[m];
   }
+  if (any_rotate) store_slice_transposed(pi_sl, sm.piT, threadIdx.x);
+  if (any_proj) store_slice_transposed(s_sl, sm.sT, threadIdx.x);
+  __syncthreads();
 
   // ---- RoPE (keys) and rotation
   if (!is_v && !rotated) {
@@ -338,15 +361,17 @@ __global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, int6
     // pair (a, b): x'_a = x_a c - x_b s, x'_b = x_a s + x_b c
     x = first ? (x * cs.x - xp * cs.y) : (xp * cs.y + x * cs.x);
   }
+  float* xs = sm.x[wave];
+  float* rs = sm.r[wave];
   if (rotate) {
-    ws->x[i] = x;
+    xs[i] = x;
     wave_sync_lds();
-    x = row_dot(prow, ws->x);
-    wave_sync_lds();   // ws->x is rewritten by quantize_wave
+    x = row_dot_t(sm.piT, xs, i);
+    wave_sync_lds();   // xs is rewritten by quantize_wave
   }
 
   uint32_t n16, g16;
-  const uint32_t nib = quantize_wave(x, c, t, srow, sign_mode, ws, i, &n16, &g16);
+  const uint32_t nib = quantize_wave(x, L, sm.sT, sign_mode, xs, rs, i, &n16, &g16);
   const int64_t tile = slot >> 6;
   const int r = (int)(slot & 63);
   if (!is_v) {
@@ -381,11 +406,11 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t st) {
     else
       hipLaunchKernelGGL(quantize_tiles_kernel<false>, grid, dim3(128), lds, st, a);
   } else {
-    const int64_t total = (int64_t)a.nlayers * a.B * a.T * a.H;
+    const uint32_t total = (uint32_t)((int64_t)a.nlayers * a.B * a.T * a.H);
     if (f16)
-      hipLaunchKernelGGL(quantize_vectors_kernel<true>, dim3((unsigned)total), dim3(128), 0, st, a, total);
+      hipLaunchKernelGGL(quantize_vectors_kernel<true>, dim3(total), dim3(128), 0, st, a, total);
     else
-      hipLaunchKernelGGL(quantize_vectors_kernel<false>, dim3((unsigned)total), dim3(128), 0, st, a, total);
+      hipLaunchKernelGGL(quantize_vectors_kernel<false>, dim3(total), dim3(128), 0, st, a, total);
   }
   return hipGetLastError();
 }
