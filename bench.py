@@ -44,6 +44,9 @@ def parse():
                     help="only run a plain device copy of this many MiB (counter calibration)")
     ap.add_argument("--decode-only", action="store_true",
                     help="time K graph-captured decode launches only (for profiling)")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch the K timed steps one by one instead of as one HIP graph "
+                         "(for counter collection)")
     return ap.parse_args()
 
 
@@ -62,13 +65,17 @@ def main():
     torch.cuda.set_device(dev)
 
     if args.copy_probe:
+        # One elementwise kernel that reads n bytes and writes n bytes (int32
+        # negation): the known traffic against which FETCH_SIZE and WRITE_SIZE
+        # are scaled.
         n = args.copy_probe * 2 ** 20
-        a = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        a = torch.ones(n // 4, dtype=torch.int32, device=dev)
         b = torch.empty_like(a)
-        for _ in range(3):
-            b.copy_(a)
         torch.cuda.synchronize()
-        print(json.dumps({"copy_probe_bytes": n}))
+        for _ in range(3):
+            torch.neg(a, out=b)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": n, "copy_probe_bytes_written": n}))
         return
 
     wl = synth.WORKLOADS[args.workload]
@@ -136,6 +143,12 @@ def main():
     eager_out = reps[0]["out"].clone()
 
     K = args.steps
+    if args.eager:
+        for s in range(K):
+            (attend if args.decode_only else step)(s % R)
+        torch.cuda.synchronize()
+        print(json.dumps({"eager_steps": K, "decode_only": bool(args.decode_only)}))
+        return
     stream = torch.cuda.Stream(device=dev)
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=stream):
@@ -236,7 +249,7 @@ def cpu_baseline(tq, params, rep, S, lut, pi, q, L, H, slots, n_ctx, seconds):
         nu = max(1, int(seconds / probe * min(32, L * H)))
         sample = np.arange(min(nu, L * H))
         units_per_run = len(sample)
-    while t_total < seconds and runs < 20:
+    while t_total < seconds:
         t0 = time.perf_counter()
         oracle.decode(oc, 1, cs, qf, [n_ctx - 1], [0], [n_ctx], pi, lut, lut, S, units=sample)
         t_total += time.perf_counter() - t0

@@ -51,6 +51,12 @@
 extern "C" {
 #endif
 
+/* Every entry point below is exported; everything else in the library is
+ * hidden (it is built with -fvisibility=hidden). */
+#ifndef TQ_API
+#define TQ_API __attribute__((visibility("default")))
+#endif
+
 /* ---- status codes ------------------------------------------------------ */
 typedef int32_t tq_status;
 #define TQ_OK             0
@@ -115,13 +121,13 @@ typedef struct tq_cache {
  * (72 bytes per slot per head; the memory accounting of Table 4 in Sec. 5.2
  * counts the same 3-bit codes in 4-bit containers plus 1-bit K signs).
  * Returns -1 for negative arguments. */
-int64_t tq_cache_bytes(int32_t num_layers, int32_t num_heads, int64_t slots);
+TQ_API int64_t tq_cache_bytes(int32_t num_layers, int32_t num_heads, int64_t slots);
 
 /* RoPE cos/sin table (Eq. 2). For position p < positions and pair m < 32:
  *   theta_m = base^(-2m/64),  a = p * theta_m  (both in double precision),
  *   cs[(p*32 + m)*2 + 0] = (float)cos(a),  cs[(p*32 + m)*2 + 1] = (float)sin(a).
  * cs: device, positions*64 floats, 16-byte aligned. base > 0 (10000 for ESM-2). */
-tq_status tq_rope_table(float* cs, int32_t positions, double base, void* stream);
+TQ_API tq_status tq_rope_table(float* cs, int32_t positions, double base, void* stream);
 
 /* Prefill-side quantizer (Sec. 3.1 prefill steps 1, 3, 4; Sec. 3.3; Sec. 3.4;
  * Sec. 4.2). For every layer l in [layer0, layer0+nlayers), sequence b < B,
@@ -150,7 +156,7 @@ tq_status tq_rope_table(float* cs, int32_t positions, double base, void* stream)
  *   qjl_s  device [64][64] fp32 Gaussian projection S (ignored with TQ_QJL_PAPER).
  *   ebar   unused by the quantizer (may be NULL).
  */
-tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache,
+TQ_API tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache,
                            const void* k, const void* v,
                            int32_t B, int32_t T, int32_t layer0, int32_t nlayers,
                            const int32_t* pos0, const int64_t* slot0,
@@ -181,7 +187,7 @@ tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache,
  *           first use; every call leaves it zero-filled again.
  *           Calls that share a workspace must be ordered on one stream.
  */
-tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache,
+TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache,
                            const void* q, int32_t B, int32_t layer0, int32_t nlayers,
                            const int32_t* q_pos, const int64_t* seq_slot0,
                            const int32_t* seq_len, int32_t max_len,
@@ -191,7 +197,7 @@ tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache,
                            void* stream);
 
 /* Workspace bytes tq_decode_attend needs for these sizes (0 if none). */
-size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B,
+TQ_API size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B,
                                  int32_t nlayers, int32_t max_len);
 
 /* Head-wise rotation calibration (Sec. 3.2): for each head, X is the
@@ -203,14 +209,14 @@ size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B,
  *   pi_out   device [nheads][64][64] fp32.
  *   sing_out device [nheads][64] fp32 singular values, or NULL.
  */
-tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal,
+TQ_API tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal,
                                 float* pi_out, float* sing_out, void* stream);
 
 /* Message of the last failing call on this thread ("" if none). */
-const char* tq_last_error(void);
+TQ_API const char* tq_last_error(void);
 
 /* Library version string. */
-const char* tq_version(void);
+TQ_API const char* tq_version(void);
 
 #ifdef __cplusplus
 }

@@ -23,7 +23,7 @@ ARCH = os.environ.get("TQ_OFFLOAD_ARCH", "gfx950")
 
 CFLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
-    "-ffp-contract=off", "-fno-fast-math",
+    "-ffp-contract=off", "-fno-fast-math", "-fvisibility=hidden",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-result",
 ]
