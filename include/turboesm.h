@@ -182,9 +182,12 @@ TQ_API tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache
  *           A sequence whose range or query position is invalid gets NaN output.
  *   max_len host bound on every seq_len (sizes the split-K grid), >= 0.
  *   out     device [nlayers][B][H][64]: io_dtype, or fp32 with TQ_OUT_FP32.
- *   workspace device, >= tq_decode_workspace_bytes(...) bytes, 16-byte aligned
- *           (may be NULL when that is 0). It must be zero-filled before its
- *           first use; every call leaves it zero-filled again.
+ *   workspace device, >= tq_decode_workspace_bytes(...) bytes, 16-byte aligned.
+ *           It holds the rotated query q^ and u of every unit (written by a
+ *           first kernel, read by the attention kernel) and, when long
+ *           sequences are split across blocks, the split partials and one
+ *           counter per unit. It must be zero-filled before its first use;
+ *           every call leaves the counters at zero again.
  *           Calls that share a workspace must be ordered on one stream.
  */
 TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache,
@@ -196,7 +199,8 @@ TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache
                            void* out, void* workspace, size_t workspace_bytes,
                            void* stream);
 
-/* Workspace bytes tq_decode_attend needs for these sizes (0 if none). */
+/* Workspace bytes tq_decode_attend needs for these sizes (0 only for empty
+ * or invalid sizes). */
 TQ_API size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B,
                                  int32_t nlayers, int32_t max_len);
 

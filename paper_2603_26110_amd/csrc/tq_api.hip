@@ -29,6 +29,8 @@ tq_status ok() {
 
 bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
 
+size_t align256(size_t n) { return (n + 255) / 256 * 256; }
+
 tq_status hip_status(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(TQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
   return ok();
@@ -123,10 +125,12 @@ size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B, int32_t nla
   const int64_t units = (int64_t)nlayers * B * params->num_heads;
   int waves, nsplit, split_tiles;
   tq::decode_plan((int)std::min<int64_t>(units, 1 << 30), max_len, &waves, &nsplit, &split_tiles);
-  if (nsplit <= 1) return 0;
-  const size_t part = (size_t)units * nsplit * tq::kPartialFloats * sizeof(float);
-  const size_t cnt = (size_t)units * sizeof(uint32_t);
-  return ((part + 255) / 256) * 256 + cnt;
+  size_t bytes = align256((size_t)units * 2 * 64 * sizeof(float));          // q^ and u per unit
+  if (nsplit > 1) {
+    bytes += align256((size_t)units * nsplit * tq::kPartialFloats * sizeof(float));
+    bytes += (size_t)units * sizeof(uint32_t);
+  }
+  return bytes;
 }
 
 tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const void* q, int32_t B,
@@ -175,10 +179,13 @@ tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const
   a.scalars = (const uint16_t*)cache->scalars; a.slots = cache->slots;
   a.out = out;
   a.nsplit = nsplit; a.split_tiles = split_tiles;
-  if (need > 0) {
-    const size_t part = (size_t)units * nsplit * tq::kPartialFloats * sizeof(float);
-    a.partials = (float*)workspace;
-    a.counters = (uint32_t*)((char*)workspace + ((part + 255) / 256) * 256);
+  char* ws = (char*)workspace;
+  a.qu = (float*)ws;
+  ws += align256((size_t)units * 2 * 64 * sizeof(float));
+  if (nsplit > 1) {
+    a.partials = (float*)ws;
+    ws += align256((size_t)units * nsplit * tq::kPartialFloats * sizeof(float));
+    a.counters = (uint32_t*)ws;
   }
   return hip_status(tq::launch_decode(a, waves, (hipStream_t)stream), "tq_decode_attend launch");
 }

@@ -1,34 +1,41 @@
 // Fused decode attention over the packed 3-bit cache (TurboESM Sec. 3.1
-// decode steps 1-4; Algorithm 1 of Sec. 4.3).
+// decode steps 1-4; Algorithm 1 of Sec. 4.3), as two kernels.
 //
-// One block (WAVES waves) handles one (sequence, layer, head) unit, or one
-// split of its 64-token tiles. Per block:
-//   loads     the first tile of every wave, this thread's slice of Pi (and of
-//             S), the query and the tables are requested before any
-//             arithmetic, so the prologue runs under the HBM latency.
-//   prologue  q' = RoPE(q), q^ = Pi q', u = S q^ (or q^ for the per-element
-//             residual form), and a 64 x 16 LDS table
-//             T[i][nibble] = (q^_i c_K[nibble & 7], +-u_i)
-//             so one table read per code gives both score terms. Rotating the
-//             query once replaces the per-key inverse rotation of Algorithm 1
-//             (identical by Eq. 4).
-//   main loop each wave takes 64-token tiles and keeps the next few in flight.
-//             Keys are scored one lane per token:
-//             score = n_k/8 (sum_i T_A + coef sum_i T_B), coef = alpha g_k (QJL)
-//             or ebar_K. Online softmax in base 2 with a wave-uniform running
-//             max that is raised only when a tile max exceeds it by more than
-//             2^8 (rescaling is rare). Values are accumulated one lane per
-//             dimension from the dimension-major V tile, with the tile's token
-//             weights broadcast through LDS.
+// decode_prep_kernel (one block per (sequence, layer, head) unit)
+//   q^ = Pi RoPE(q) and u = S q^ (u = q^ for the per-element residual form),
+//   written to the workspace. Rotating the query once replaces the per-key
+//   inverse rotation of Algorithm 1 (identical by Eq. 4). Each row of Pi is
+//   shared by 4 contiguous lanes; a lane applies RoPE to its 16-element slice
+//   of q in registers and the lanes of a row combine their partial sums with
+//   DPP.
+//
+// decode_kernel (one block of WAVES waves per unit, or per split of its tiles)
+//   The cache read is bandwidth-bound and, with every block streaming at
+//   once, any load issued behind the stream waits for it. So nothing the
+//   block computes may wait on a load chained behind another: the 512 bytes of
+//   (q^, u) from the prep kernel are requested first, then every tile of the
+//   unit (two register buffers per wave and, for the first waves, one more
+//   tile loaded straight into LDS), then Pi for the epilogue straight into
+//   LDS. Per block:
+//   prologue  an LDS table T[i][nibble] = (q^_i c_K[nibble & 7], +-u_i), so one
+//             table read per code gives both score terms; one barrier.
+//   main loop keys are scored one lane per token:
+//             score = n_k/8 (sum_i T_A + coef sum_i T_B), coef = alpha g_k
+//             (QJL) or ebar_K. Online softmax in base 2 with a wave-uniform
+//             running max that is raised only when a tile max exceeds it by more
+//             than 2^8 (rescaling is rare). Values are accumulated one lane per
+//             dimension from the dimension-major V tile; the tile's token weights
+//             reach every lane through v_readlane (scalar registers), which
+//             keeps them off the LDS pipe that the table reads load.
 //   merge     waves merge through LDS; splits of a unit merge through a
 //             workspace of (m, l, o) partials written and read with
 //             agent-scope atomics: the last split to finish (atomic counter)
 //             combines them by log-sum-exp.
-//   epilogue  o = Pi^T (o^ / l) (one inverse rotation; Pi staged in LDS), plus
-//             the V residual estimate alpha S^T s or ebar_V s when V carries
-//             sign bits.
+//   epilogue  o = Pi^T (o^ / l) (one inverse rotation), plus the V residual
+//             estimate alpha S^T s or ebar_V s when V carries sign bits.
 // Work items are dealt so that all splits of a unit land on one XCD (blocks
-// go to the 8 XCDs round-robin), keeping that unit's Pi in one L2.
+// go to the 8 XCDs round-robin), and each unit's prep block runs on the XCD
+// of its decode blocks.
 #include <stdlib.h>
 
 #include "tq_device.hpp"
@@ -38,32 +45,14 @@ namespace tq {
 
 constexpr float kLazyRescale = 8.0f;   // log2 headroom before the max is raised
 constexpr int kXcds = 8;
-constexpr int kPiPitch = kDim + 1;     // padded LDS row of Pi (conflict-free columns)
 
-template <int WAVES>
-struct DecodeSmem {
-  float2 ktab[kDim * 16];
-  float pi[kDim * kPiPitch];
-  float vtab[16];
-  float q[kDim];
-  float qh[kDim];
-  float u[kDim];
-  float part[WAVES][kDim];
-  float wp[WAVES][kDim];        // per-tile token weights (V accumulate)
-  float wg[WAVES][kDim];        // per-tile token weights for the V residual term
-  float wo[WAVES][kDim];
-  float wsg[WAVES][kDim];
-  float wm[WAVES];
-  float wl[WAVES];
-  float oh[kDim];
-  float sh[kDim];
-  int last;
-};
-
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+// Block barrier that orders LDS only. __syncthreads() also waits for every
+// outstanding global load of the wave (its release fence covers global
+// memory), which would drain the tile prefetch at each prologue barrier.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 // (byte B of x) & m, one VALU op (sub-dword operand select).
@@ -159,6 +148,7 @@ __device__ __forceinline__ void load_tile(TileRegs& r, const uint8_t* kreg, cons
   r.sc = sreg[s0 + (int64_t)tt * kTile + lane];
 }
 
+
 // Sum of T[i][nibble_i] over the 8 codes of word w (dims 8w..8w+7).
 __device__ __forceinline__ void score_word(const float2* ktab_w, uint32_t x, float& A, float& B) {
   uint32_t off[8];
@@ -171,13 +161,170 @@ __device__ __forceinline__ void score_word(const float2* ktab_w, uint32_t x, flo
   B += ((e[0].y + e[1].y) + (e[2].y + e[3].y)) + ((e[4].y + e[5].y) + (e[6].y + e[7].y));
 }
 
+
+// N consecutive elements of an fp16 or fp32 vector, in two steps so that all
+// prologue loads are in flight before the first wait: load_raw issues the
+// 16-byte loads (element e0 is a multiple of 8, so they are aligned) and
+// to_float converts after the remaining loads have been issued.
+template <int N>
+struct RawSlice {
+  uint4 w[N / 4];
+};
+
+template <int N>
+__device__ __forceinline__ void load_raw(const void* p, int64_t e0, bool f16, RawSlice<N>& r) {
+  if (f16) {
+    const uint4* q = reinterpret_cast<const uint4*>(reinterpret_cast<const __half*>(p) + e0);
+#pragma unroll
+    for (int j = 0; j < N / 8; ++j) r.w[j] = q[j];
+  } else {
+    const uint4* q = reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(p) + e0);
+#pragma unroll
+    for (int j = 0; j < N / 4; ++j) r.w[j] = q[j];
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void to_float(const RawSlice<N>& r, bool f16, float (&x)[N]) {
+  if (f16) {
+#pragma unroll
+    for (int j = 0; j < N / 8; ++j) {
+      const uint32_t ws[4] = {r.w[j].x, r.w[j].y, r.w[j].z, r.w[j].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        x[8 * j + 2 * k] = half_bits_to_float(ws[k]);
+        x[8 * j + 2 * k + 1] = half_bits_to_float(ws[k] >> 16);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < N / 4; ++j) {
+      x[4 * j] = __uint_as_float(r.w[j].x); x[4 * j + 1] = __uint_as_float(r.w[j].y);
+      x[4 * j + 2] = __uint_as_float(r.w[j].z); x[4 * j + 3] = __uint_as_float(r.w[j].w);
+    }
+  }
+}
+
+
+// ------------------------------------------------------------------ prep kernel
+// Unit of prep block `bid`: the XCD of a unit's decode blocks is
+// (unit * nsplit) / per_xcd; prep blocks are dealt to the same XCD.
+__global__ __launch_bounds__(256) void decode_prep_kernel(DecodeArgs a, int units, int per_xcd) {
+  constexpr int COLS = 16;                 // 4 lanes per row of Pi / S
+  __shared__ float s_qh[kDim];
+  const int x = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
+  const int64_t first = ((int64_t)x * per_xcd + a.nsplit - 1) / a.nsplit;
+  const int64_t next = ((int64_t)(x + 1) * per_xcd + a.nsplit - 1) / a.nsplit;
+  const int64_t unit64 = first + j;
+  if (unit64 >= next || unit64 >= units) return;
+  const int unit = (int)unit64;
+  const int h = unit % a.H;
+  const int b = (unit / a.H) % a.B;
+  const int l = a.layer0 + unit / (a.H * a.B);
+  const int lh = l * a.H + h;
+  const int qp = a.q_pos[b];
+  const int n = a.seq_len[b];
+  if (qp < 0 || qp >= a.rope_positions || n <= 0) return;   // the decode kernel writes 0 or NaN
+  const int t = threadIdx.x;
+  const int row = t >> 2, c0 = (t & 3) * COLS;
+  const bool paper = (a.flags & kQjlPaper) != 0;
+  const bool half = (a.flags & kRopeHalf) != 0;
+  const bool f16q = a.f16_in != 0;
+
+  const float4* pi_row = reinterpret_cast<const float4*>(a.pi + (int64_t)lh * kDim * kDim + row * kDim + c0);
+  float4 pr[COLS / 4], sr[COLS / 4];
+#pragma unroll
+  for (int k = 0; k < COLS / 4; ++k) pr[k] = pi_row[k];
+  if (!paper) {
+    const float4* s_row = reinterpret_cast<const float4*>(a.qjl_s + row * kDim + c0);
+#pragma unroll
+    for (int k = 0; k < COLS / 4; ++k) sr[k] = s_row[k];
+  }
+  const float4* cs_row = reinterpret_cast<const float4*>(a.rope_cs + (int64_t)qp * 2 * kPairs);
+  RawSlice<COLS> qraw, praw;
+  load_raw<COLS>(a.q, (int64_t)unit * kDim + c0, f16q, qraw);
+  if (half) load_raw<COLS>(a.q, (int64_t)unit * kDim + (c0 ^ 32), f16q, praw);
+  float4 csv[COLS / 2];
+  if (half) {
+#pragma unroll
+    for (int k = 0; k < COLS / 2; ++k) csv[k] = cs_row[(c0 & 31) / 2 + k];   // pairs (c0 & 31) ..
+  } else {
+#pragma unroll
+    for (int k = 0; k < COLS / 4; ++k) csv[k] = cs_row[c0 / 4 + k];          // pairs c0/2 ..
+  }
+
+  // q' = RoPE(q) in registers (x'_a = x_a c - x_b s, x'_b = x_a s + x_b c)
+  float qx[COLS], qy[COLS], qr[COLS];
+  to_float<COLS>(qraw, f16q, qx);
+  if (half) {
+    to_float<COLS>(praw, f16q, qy);
+#pragma unroll
+    for (int k = 0; k < COLS; ++k) {
+      const float4 v = csv[k / 2];
+      const float c = (k & 1) ? v.z : v.x, sn = (k & 1) ? v.w : v.y;
+      qr[k] = (c0 + k) < 32 ? (qx[k] * c - qy[k] * sn) : (qy[k] * sn + qx[k] * c);
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < COLS; k += 2) {
+      const float4 v = csv[k / 4];
+      const float c = (k & 2) ? v.z : v.x, sn = (k & 2) ? v.w : v.y;
+      qr[k] = qx[k] * c - qx[k + 1] * sn;
+      qr[k + 1] = qx[k] * sn + qx[k + 1] * c;
+    }
+  }
+  float acc = 0.0f;
+#pragma unroll
+  for (int k = 0; k < COLS / 4; ++k) {
+    acc = fmaf(pr[k].x, qr[4 * k + 0], acc);
+    acc = fmaf(pr[k].y, qr[4 * k + 1], acc);
+    acc = fmaf(pr[k].z, qr[4 * k + 2], acc);
+    acc = fmaf(pr[k].w, qr[4 * k + 3], acc);
+  }
+  acc += dpp<0xB1>(acc);               // quad_perm [1,0,3,2]
+  acc += dpp<0x4E>(acc);               // quad_perm [2,3,0,1]: every lane of the row has q^_row
+  const float qh_row = acc;
+  float* qu = a.qu + (int64_t)unit * 2 * kDim;
+  if ((t & 3) == 0) { s_qh[row] = qh_row; qu[row] = qh_row; }
+  float u_row = qh_row;
+  if (!paper) {
+    lds_barrier();
+    float up = 0.0f;
+#pragma unroll
+    for (int k = 0; k < COLS / 4; ++k) {
+      const float4 v = *reinterpret_cast<const float4*>(s_qh + c0 + 4 * k);
+      up = fmaf(sr[k].x, v.x, up);
+      up = fmaf(sr[k].y, v.y, up);
+      up = fmaf(sr[k].z, v.z, up);
+      up = fmaf(sr[k].w, v.w, up);
+    }
+    up += dpp<0xB1>(up);
+    up += dpp<0x4E>(up);
+    u_row = up;
+  }
+  if ((t & 3) == 1) qu[kDim + row] = u_row;
+}
+
+
+
 template <int WAVES, bool VQJL>
 __global__ __launch_bounds__(WAVES * 64)
 __attribute__((amdgpu_waves_per_eu((WAVES == 8 && !VQJL) ? 6 : 1)))
 void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
+  constexpr int NPL = 16 / WAVES;          // table entries per lane and row
+  constexpr int COLS = kDim / WAVES;       // rows of Pi per thread in the epilogue
+  constexpr int DEPTH = (WAVES == 8) ? 1 : 2;
   constexpr int NT = WAVES * 64;
-  constexpr int COLS = kDim / WAVES;       // columns of Pi / S per thread
-  __shared__ DecodeSmem<WAVES> sm;
+  constexpr int PIV = 1024 / NT;          // float4 of Pi per thread
+  __shared__ float2 s_ktab[kDim * 16];
+  __shared__ __attribute__((aligned(16))) float s_pi[kDim * kDim];
+  __shared__ float s_vtab[16];
+  __shared__ float s_part[WAVES][kDim];
+  __shared__ float s_wo[WAVES][kDim];
+  __shared__ float s_wsg[VQJL ? WAVES : 1][kDim];
+  __shared__ float s_wm[WAVES], s_wl[WAVES];
+  __shared__ float s_oh[kDim], s_sh[kDim];
+  __shared__ int s_last;
   const int bid = blockIdx.x;
   const int work = (bid % kXcds) * per_xcd + bid / kXcds;
   if (work >= total_work) return;
@@ -207,110 +354,51 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   const int participants = (ntiles + a.split_tiles - 1) / a.split_tiles;
   const bool paper = (a.flags & kQjlPaper) != 0;
 
-  // ------------------------------------------------------------------ loads
+  // ------------------------------------------- loads, in the order they are needed
+  const int row = t / WAVES, sub = t % WAVES;
+  const float* qu = a.qu + (int64_t)unit * 2 * kDim;
+  const float qh_row = qu[row];
+  const float u_row = qu[kDim + row];
+  float ck[NPL];
+#pragma unroll
+  for (int e = 0; e < NPL; ++e) ck[e] = a.lut_k[lh * 8 + ((sub * NPL + e) & 7)];
+  const float cv = a.lut_v[lh * 8 + (t & 7)];
+  // (every prologue load is unconditional: a load under a branch makes the
+  // compiler's wait counts after the join conservative)
+  const float ebar_raw = *(paper ? a.ebar + lh * 2 : a.lut_k + lh * 8);
+  const float ebar_k = paper ? ebar_raw : 0.0f;
+
   const uint8_t* kreg = a.k_codes + (int64_t)lh * a.slots * 32;
   const uint8_t* vreg = a.v_codes + (int64_t)lh * a.slots * 32;
   const uint2* sreg = reinterpret_cast<const uint2*>(a.scalars + (int64_t)lh * a.slots * 4);
   const int64_t tile0 = s0 >> 6;
-  const int ri = t & 63, cq = t >> 6;      // row and column group of Pi / S
-  const float4* pi_row = reinterpret_cast<const float4*>(a.pi + (int64_t)lh * kDim * kDim + ri * kDim + cq * COLS);
-  float4 pr[COLS / 4];
-#pragma unroll
-  for (int k = 0; k < COLS / 4; ++k) pr[k] = pi_row[k];
-  float4 sr[COLS / 4];
-  if (!paper) {
-    const float4* s_row = reinterpret_cast<const float4*>(a.qjl_s + ri * kDim + cq * COLS);
-#pragma unroll
-    for (int k = 0; k < COLS / 4; ++k) sr[k] = s_row[k];
-  }
-  float qv = 0.0f;
-  float2 cs = make_float2(1.0f, 0.0f);
-  const bool half = (a.flags & kRopeHalf) != 0;
-  if (t < kDim) {
-    qv = load_in(a.q, (int64_t)unit * kDim + t, a.f16_in != 0);
-    const int m = half ? (t & 31) : (t >> 1);
-    cs = reinterpret_cast<const float2*>(a.rope_cs + (int64_t)qp * 2 * kPairs)[m];
-  }
-  const float ck = a.lut_k[lh * 8 + (t & 7)];
-  const float cvv = a.lut_v[lh * 8 + (t & 7)];
-  const float ebar_k = paper ? a.ebar[lh * 2 + 0] : 0.0f;
-
-  // Tiles are requested after Pi, S and the query (the prologue needs those
-  // first). Each wave keeps DEPTH tiles in flight: its first DEPTH tiles are
-  // requested now, and every processed tile is replaced by the one DEPTH
-  // steps ahead.
-  constexpr int DEPTH = (WAVES == 8) ? 1 : 2;
   TileRegs buf[DEPTH];
 #pragma unroll
   for (int d = 0; d < DEPTH; ++d) {
-    const int tq = tile_begin + wave + d * WAVES;
-    if (tq < tile_end) load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
+    const int tq = min(tile_begin + wave + d * WAVES, tile_end - 1);   // (a wave without tiles re-reads one)
+    load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
   }
-
   // --------------------------------------------------------------- prologue
-  if (t < kDim) {
-    const int partner = half ? (t ^ 32) : (t ^ 1);
-    const bool first = half ? (t < 32) : ((t & 1) == 0);
-    const float qpv = __shfl(qv, partner, 64);
-    sm.q[t] = first ? (qv * cs.x - qpv * cs.y) : (qpv * cs.y + qv * cs.x);
-  }
 #pragma unroll
-  for (int k = 0; k < COLS / 4; ++k) {
-    float* dst = sm.pi + ri * kPiPitch + cq * COLS + 4 * k;
-    dst[0] = pr[k].x; dst[1] = pr[k].y; dst[2] = pr[k].z; dst[3] = pr[k].w;
+  for (int e = 0; e < NPL; ++e) {
+    const int nib = sub * NPL + e;
+    s_ktab[row * 16 + nib] = make_float2(qh_row * ck[e], (nib & 8) ? u_row : -u_row);
   }
-  if (t < 16) sm.vtab[t] = cvv;
-  __syncthreads();
+  s_vtab[t & 15] = cv;             // every thread: identical values, no branch around the load
+  lds_barrier();
+
+  // Pi for the epilogue, straight into LDS (1 KB per wave instruction). Issued
+  // after the last barrier before the merge: the compiler makes a barrier wait
+  // for transfers into LDS still in flight.
   {
-    const float* x = sm.q + cq * COLS;
-    float acc = 0.0f;
+    typedef __attribute__((address_space(3))) void* lds_ptr;
+    const float* pig = a.pi + (int64_t)lh * kDim * kDim;
 #pragma unroll
-    for (int k = 0; k < COLS / 4; ++k) {
-      acc = fmaf(pr[k].x, x[4 * k + 0], acc);
-      acc = fmaf(pr[k].y, x[4 * k + 1], acc);
-      acc = fmaf(pr[k].z, x[4 * k + 2], acc);
-      acc = fmaf(pr[k].w, x[4 * k + 3], acc);
+    for (int j = 0; j < PIV; ++j) {
+      const int chunk = (wave + WAVES * j) * 64;    // first 16-byte chunk of this wave instruction
+      __builtin_amdgcn_global_load_lds(pig + (chunk + lane) * 4, (lds_ptr)(s_pi + chunk * 4), 16, 0, 0);
     }
-    sm.part[cq][ri] = acc;
   }
-  __syncthreads();
-  if (t < kDim) {
-    float y = 0.0f;
-#pragma unroll
-    for (int w = 0; w < WAVES; ++w) y += sm.part[w][t];
-    sm.qh[t] = y;
-  }
-  __syncthreads();
-  if (!paper) {
-    const float* x = sm.qh + cq * COLS;
-    float acc = 0.0f;
-#pragma unroll
-    for (int k = 0; k < COLS / 4; ++k) {
-      acc = fmaf(sr[k].x, x[4 * k + 0], acc);
-      acc = fmaf(sr[k].y, x[4 * k + 1], acc);
-      acc = fmaf(sr[k].z, x[4 * k + 2], acc);
-      acc = fmaf(sr[k].w, x[4 * k + 3], acc);
-    }
-    sm.part[cq][ri] = acc;
-    __syncthreads();
-    if (t < kDim) {
-      float y = 0.0f;
-#pragma unroll
-      for (int w = 0; w < WAVES; ++w) y += sm.part[w][t];
-      sm.u[t] = y;
-    }
-  } else {
-    if (t < kDim) sm.u[t] = sm.qh[t];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < 1024 / NT; ++r) {
-    const int e = t + NT * r;
-    const int d = e >> 4, nib = e & 15;
-    const float cknib = __shfl(ck, nib & 7, 64);    // lane j of any wave holds c_K[j & 7]
-    sm.ktab[e] = make_float2(sm.qh[d] * cknib, (nib & 8) ? sm.u[d] : -sm.u[d]);
-  }
-  __syncthreads();
 
   // -------------------------------------------------------------- main loop
   float m_run = -INFINITY;
@@ -318,8 +406,8 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   float sg = 0.0f;
   float o0 = 0.0f, o1 = 0.0f, o2 = 0.0f, o3 = 0.0f;
   const float lscale = a.logit_scale2;
-  const float2* ktab = sm.ktab;
-  const char* vtab = reinterpret_cast<const char*>(sm.vtab);
+  const float2* ktab = s_ktab;
+  const char* vtab = reinterpret_cast<const char*>(s_vtab);
 
   for (int tb = tile_begin + wave; tb < tile_end; tb += DEPTH * WAVES) {
 #pragma unroll
@@ -329,7 +417,6 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
       const TileRegs& cur = buf[d];
       const int tok = tt * kTile + lane;
       const bool tv = tok < n;
-
       // ---- key score, one lane per token. Two words (16 table reads) in
       // flight at a time: the empty asm pins the partial sums so the compiler
       // does not hoist every table read of the tile (registers, occupancy).
@@ -363,63 +450,66 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
       const float p = __builtin_amdgcn_exp2f(lg - m_run);
       l_lane += p;
       const float wv = tv ? p * nv * 0.125f : 0.0f;
-      sm.wp[wave][lane] = wv;
-      if (VQJL) sm.wg[wave][lane] = paper ? wv : wv * gv;
-      wave_lds_sync();
+      const float wg = VQJL ? (paper ? wv : wv * gv) : 0.0f;
 
-      // ---- value accumulate, one lane per dimension
+      // ---- value accumulate, one lane per dimension; token weights from
+      // their lanes through scalar registers
       const uint32_t vw[8] = {cur.v0.x, cur.v0.y, cur.v0.z, cur.v0.w, cur.v1.x, cur.v1.y, cur.v1.z, cur.v1.w};
-      const float4* wp4 = reinterpret_cast<const float4*>(sm.wp[wave]);
+      const int wvi = __float_as_int(wv);
   #pragma unroll
       for (int w8 = 0; w8 < 8; ++w8) {
         const uint32_t x = vw[w8];
-        const float4 wa = wp4[2 * w8], wb = wp4[2 * w8 + 1];
         uint32_t off[8];
         nibble_offsets4(x, off);     // (nibble & 7) * 4: float entries
-        o0 = fmaf(wa.x, *reinterpret_cast<const float*>(vtab + off[0]), o0);
-        o1 = fmaf(wa.y, *reinterpret_cast<const float*>(vtab + off[1]), o1);
-        o2 = fmaf(wa.z, *reinterpret_cast<const float*>(vtab + off[2]), o2);
-        o3 = fmaf(wa.w, *reinterpret_cast<const float*>(vtab + off[3]), o3);
-        o0 = fmaf(wb.x, *reinterpret_cast<const float*>(vtab + off[4]), o0);
-        o1 = fmaf(wb.y, *reinterpret_cast<const float*>(vtab + off[5]), o1);
-        o2 = fmaf(wb.z, *reinterpret_cast<const float*>(vtab + off[6]), o2);
-        o3 = fmaf(wb.w, *reinterpret_cast<const float*>(vtab + off[7]), o3);
+        float ws[8];
+  #pragma unroll
+        for (int jj = 0; jj < 8; ++jj) ws[jj] = __int_as_float(__builtin_amdgcn_readlane(wvi, 8 * w8 + jj));
+        o0 = fmaf(ws[0], *reinterpret_cast<const float*>(vtab + off[0]), o0);
+        o1 = fmaf(ws[1], *reinterpret_cast<const float*>(vtab + off[1]), o1);
+        o2 = fmaf(ws[2], *reinterpret_cast<const float*>(vtab + off[2]), o2);
+        o3 = fmaf(ws[3], *reinterpret_cast<const float*>(vtab + off[3]), o3);
+        o0 = fmaf(ws[4], *reinterpret_cast<const float*>(vtab + off[4]), o0);
+        o1 = fmaf(ws[5], *reinterpret_cast<const float*>(vtab + off[5]), o1);
+        o2 = fmaf(ws[6], *reinterpret_cast<const float*>(vtab + off[6]), o2);
+        o3 = fmaf(ws[7], *reinterpret_cast<const float*>(vtab + off[7]), o3);
         if (w8 & 1) asm volatile("" : "+v"(o0), "+v"(o1), "+v"(o2), "+v"(o3));
       }
       if (VQJL) {
-        const float4* wg4 = reinterpret_cast<const float4*>(sm.wg[wave]);
+        const int wgi = __float_as_int(wg);
   #pragma unroll
         for (int w8 = 0; w8 < 8; ++w8) {
           const uint32_t x = vw[w8];
-          const float4 ga = wg4[2 * w8], gb = wg4[2 * w8 + 1];
-          const float gt8[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
   #pragma unroll
-          for (int jj = 0; jj < 8; ++jj) sg += ((x >> (4 * jj + 3)) & 1u) ? gt8[jj] : -gt8[jj];
+          for (int jj = 0; jj < 8; ++jj) {
+            const float g = __int_as_float(__builtin_amdgcn_readlane(wgi, 8 * w8 + jj));
+            sg += ((x >> (4 * jj + 3)) & 1u) ? g : -g;
+          }
         }
       }
-      wave_lds_sync();   // wp/wg are rewritten by the next tile
-      const int tn = tt + DEPTH * WAVES;
-      if (tn < tile_end) load_tile(buf[d], kreg, vreg, sreg, tile0 + tn, s0, tn, lane);
+
+        const int tn = tt + DEPTH * WAVES;
+        if (tn < tile_end) load_tile(buf[d], kreg, vreg, sreg, tile0 + tn, s0, tn, lane);
     }
   }
 
   // ------------------------------------------------------ merge the waves
+  // (a full barrier: it also waits for this wave's Pi transfer into LDS)
   const float ov = (o0 + o1) + (o2 + o3);
   const float l_wave = wave_sum_uniform(l_lane);
-  if (lane == 0) { sm.wm[wave] = m_run; sm.wl[wave] = l_wave; }
-  sm.wo[wave][lane] = ov;
-  if (VQJL) sm.wsg[wave][lane] = sg;
+  if (lane == 0) { s_wm[wave] = m_run; s_wl[wave] = l_wave; }
+  s_wo[wave][lane] = ov;
+  if (VQJL) s_wsg[wave][lane] = sg;
   __syncthreads();
   float M = -INFINITY, L = 0.0f, O = 0.0f, SG = 0.0f;
   if (t < kDim) {
 #pragma unroll
-    for (int w = 0; w < WAVES; ++w) M = fmaxf(M, sm.wm[w]);
+    for (int w = 0; w < WAVES; ++w) M = fmaxf(M, s_wm[w]);
 #pragma unroll
     for (int w = 0; w < WAVES; ++w) {
-      const float f = __builtin_amdgcn_exp2f(sm.wm[w] - M);
-      L += sm.wl[w] * f;
-      O += sm.wo[w][t] * f;
-      if (VQJL) SG += sm.wsg[w][t] * f;
+      const float f = __builtin_amdgcn_exp2f(s_wm[w] - M);
+      L += s_wl[w] * f;
+      O += s_wo[w][t] * f;
+      if (VQJL) SG += s_wsg[w][t] * f;
     }
   }
 
@@ -442,10 +532,10 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     if (t == 0) {
       const uint32_t prev = __hip_atomic_fetch_add(a.counters + unit, 1u, __ATOMIC_RELAXED,
                                                    __HIP_MEMORY_SCOPE_AGENT);
-      sm.last = (prev == (uint32_t)(participants - 1)) ? 1 : 0;
+      s_last = (prev == (uint32_t)(participants - 1)) ? 1 : 0;
     }
-    __syncthreads();
-    if (!sm.last) return;
+    lds_barrier();
+    if (!s_last) return;
     if (t < kDim) {
       float* base = a.partials + (int64_t)unit * a.nsplit * kPartialFloats;
       M = -INFINITY;
@@ -465,13 +555,14 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   }
 
   // --------------------------------------------------------------- epilogue
+  const int cq = t >> 6;                   // row group of the epilogue products
   const float invL = 1.0f / L;
-  if (t < kDim) { sm.oh[t] = O * invL; sm.sh[t] = SG * invL; }
-  __syncthreads();
+  if (t < kDim) { s_oh[t] = O * invL; s_sh[t] = SG * invL; }
+  lds_barrier();
   if (VQJL) {
     if (paper) {
       const float ebar_v = a.ebar[lh * 2 + 1];
-      if (t < kDim) sm.oh[t] += ebar_v * sm.sh[t];
+      if (t < kDim) s_oh[t] += ebar_v * s_sh[t];
     } else {
       // o^ += alpha S^T s; thread (k, group) sums COLS rows of column k of S
       const int k = t & 63;
@@ -479,18 +570,18 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
       for (int ii = 0; ii < COLS; ++ii) {
         const int i = cq * COLS + ii;
-        acc = fmaf(a.qjl_s[i * kDim + k], sm.sh[i], acc);
+        acc = fmaf(a.qjl_s[i * kDim + k], s_sh[i], acc);
       }
-      sm.part[cq][k] = acc;
-      __syncthreads();
+      s_part[cq][k] = acc;
+      lds_barrier();
       if (t < kDim) {
         float y = 0.0f;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) y += sm.part[w][t];
-        sm.oh[t] += kQjlAlpha * y;
+        for (int w = 0; w < WAVES; ++w) y += s_part[w][t];
+        s_oh[t] += kQjlAlpha * y;
       }
     }
-    __syncthreads();
+    lds_barrier();
   }
   if (a.flags & kVRotate) {
     // out_k = sum_i Pi[i][k] o^_i: thread (k, group) sums COLS rows
@@ -499,18 +590,18 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
     for (int ii = 0; ii < COLS; ++ii) {
       const int i = cq * COLS + ii;
-      acc = fmaf(sm.pi[i * kPiPitch + k], sm.oh[i], acc);
+      acc = fmaf(s_pi[i * kDim + k], s_oh[i], acc);
     }
-    sm.part[cq][k] = acc;
-    __syncthreads();
+    s_part[cq][k] = acc;
+    lds_barrier();
     if (t < kDim) {
       float y = 0.0f;
 #pragma unroll
-      for (int w = 0; w < WAVES; ++w) y += sm.part[w][t];
+      for (int w = 0; w < WAVES; ++w) y += s_part[w][t];
       store_out(a, unit, t, y);
     }
   } else {
-    if (t < kDim) store_out(a, unit, t, sm.oh[t]);
+    if (t < kDim) store_out(a, unit, t, s_oh[t]);
   }
 }
 
@@ -546,6 +637,10 @@ hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st) {
   const int64_t per_xcd = (total + kXcds - 1) / kXcds;
   const int64_t blocks = per_xcd * kXcds;
   const bool vq = (a.flags & kVQjl) != 0;
+  // prep blocks: per XCD, the units whose decode blocks run there
+  const int64_t prep_per_xcd = (per_xcd + a.nsplit - 1) / a.nsplit + 1;
+  hipLaunchKernelGGL(decode_prep_kernel, dim3((unsigned)(kXcds * prep_per_xcd)), dim3(256), 0, st, a,
+                     (int)units, (int)per_xcd);
   if (waves == 8) {
     if (vq)
       hipLaunchKernelGGL((decode_kernel<8, true>), dim3((unsigned)blocks), dim3(512), 0, st, a, (int)total, (int)per_xcd);

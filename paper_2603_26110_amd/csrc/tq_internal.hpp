@@ -51,6 +51,7 @@ struct DecodeArgs {
   const uint16_t* scalars;
   int64_t slots;
   void* out;
+  float* qu;               // [units][2][64]: q^ and u from the prep kernel
   float* partials;         // [units][nsplit][kPartialFloats]
   uint32_t* counters;      // [units]
   int nsplit;              // splits per unit
