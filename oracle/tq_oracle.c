@@ -15,9 +15,11 @@
  *     (codes and sign bits), so they are written in binary32 with one fixed
  *     evaluation order: sequential fmaf chains, correctly rounded sqrtf and
  *     division. Build with -ffp-contract=off so nothing else is fused.
- *   - Packing into the cache layout (Sec. 4.2 packs 8 codes per 32-bit word;
- *     here each code is a 4-bit nibble that also holds the sign bit; key
- *     tiles are token-major, value tiles dimension-major).
+ *   - Packing into the cache layout (Sec. 4.2 packs 8 codes per 32-bit word).
+ *     Every code is handled as a 4-bit value idx | sign << 3. In a key word
+ *     the eight 3-bit indices fill bits 0..23 and the eight sign bits bits
+ *     24..31; a value word holds eight such 4-bit nibbles. Key tiles are
+ *     token-major, value tiles dimension-major.
  *   - Decode attention (Sec. 3.1 decode steps; Algorithm 1 of Sec. 4.3),
  *     fp64: a streaming online-softmax form and a two-step form that first
  *     materializes the dequantized keys and values.
@@ -211,8 +213,8 @@ void orc_quantize_vector(const float* xhat, const float* c, const float* S,
 }
 
 /* ------------------------------------------------------------------------ */
-/* Cache layout: 8 nibbles per 32-bit word (Sec. 4.2 packs 8 codes per      */
-/* 32-bit container); 64-slot tiles, 16-byte halves interleaved by slot.     */
+/* Cache layout: 8 codes per 32-bit word (Sec. 4.2 packs 8 codes per 32-bit */
+/* container); 64-slot tiles, 16-byte halves interleaved by slot.            */
 /* ------------------------------------------------------------------------ */
 
 /* K plane, token-major tiles: 16-byte half c (codes 32c..32c+31) of slot s
@@ -222,11 +224,21 @@ static int64_t k_half_offset(int64_t s, int c) {
   return tile * (TILE * 32) + ((int64_t)c * TILE + lane) * 16;
 }
 
-/* Write the 64 nibbles of one slot of the K plane. */
+/* K word of dimensions 8w..8w+7: the 3-bit index of dimension 8w+j in bits
+ * 3j..3j+2, its sign bit in bit 24+j. */
+static uint32_t k_word(const uint8_t* nib8) {
+  uint32_t word = 0;
+  for (int j = 0; j < 8; ++j) {
+    word |= (uint32_t)(nib8[j] & 7) << (3 * j);
+    word |= (uint32_t)((nib8[j] >> 3) & 1) << (24 + j);
+  }
+  return word;
+}
+
+/* Write the 64 codes (idx | sign << 3) of one slot of the K plane. */
 void orc_pack_slot(uint8_t* region, int64_t s, const uint8_t* nib) {
   for (int w = 0; w < 8; ++w) {
-    uint32_t word = 0;
-    for (int j = 0; j < 8; ++j) word |= (uint32_t)(nib[w * 8 + j] & 0xF) << (4 * j);
+    const uint32_t word = k_word(nib + 8 * w);
     uint8_t* dst = region + k_half_offset(s, w / 4) + (w % 4) * 4;
     dst[0] = (uint8_t)(word & 0xFF);
     dst[1] = (uint8_t)((word >> 8) & 0xFF);
@@ -235,13 +247,14 @@ void orc_pack_slot(uint8_t* region, int64_t s, const uint8_t* nib) {
   }
 }
 
-/* Read the 64 nibbles of one slot of the K plane. */
+/* Read the 64 codes (idx | sign << 3) of one slot of the K plane. */
 void orc_unpack_slot(const uint8_t* region, int64_t s, uint8_t* nib) {
   for (int w = 0; w < 8; ++w) {
     const uint8_t* src = region + k_half_offset(s, w / 4) + (w % 4) * 4;
     uint32_t word = (uint32_t)src[0] | ((uint32_t)src[1] << 8) |
                     ((uint32_t)src[2] << 16) | ((uint32_t)src[3] << 24);
-    for (int j = 0; j < 8; ++j) nib[w * 8 + j] = (uint8_t)((word >> (4 * j)) & 0xF);
+    for (int j = 0; j < 8; ++j)
+      nib[w * 8 + j] = (uint8_t)(((word >> (3 * j)) & 7) | (((word >> (24 + j)) & 1) << 3));
   }
 }
 

@@ -74,18 +74,6 @@ __device__ __forceinline__ uint32_t and_byte(uint32_t m, uint32_t x) {
   return r;
 }
 
-// Byte offsets of the 8 nibbles of x into a table with 8-byte entries indexed
-// by the nibble: nibble 2b comes from byte b of x << 3, nibble 2b+1 from byte
-// b of x >> 1 (each masked with 0x78 = nibble * 8).
-__device__ __forceinline__ void nibble_offsets8(uint32_t x, uint32_t (&off)[8]) {
-  const uint32_t m = 0x78u;
-  const uint32_t lo = x << 3, hi = x >> 1;
-  off[0] = and_byte<0>(m, lo); off[1] = and_byte<0>(m, hi);
-  off[2] = and_byte<1>(m, lo); off[3] = and_byte<1>(m, hi);
-  off[4] = and_byte<2>(m, lo); off[5] = and_byte<2>(m, hi);
-  off[6] = and_byte<3>(m, lo); off[7] = and_byte<3>(m, hi);
-}
-
 // Byte offsets (nibble & 7) * 4 of the 8 nibbles of x into a float table:
 // nibble 2b from byte b of x << 2, nibble 2b+1 from byte b of x >> 2 (0x1C).
 __device__ __forceinline__ void nibble_offsets4(uint32_t x, uint32_t (&off)[8]) {
@@ -149,18 +137,126 @@ __device__ __forceinline__ void load_tile(TileRegs& r, const uint8_t* kreg, cons
 }
 
 
-// Sum of T[i][nibble_i] over the 8 codes of word w (dims 8w..8w+7).
-__device__ __forceinline__ void score_word(const float2* ktab_w, uint32_t x, float& A, float& B) {
-  uint32_t off[8];
-  nibble_offsets8(x, off);
-  const char* base = reinterpret_cast<const char*>(ktab_w);
-  float2 e[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) e[j] = *reinterpret_cast<const float2*>(base + j * 128 + off[j]);
-  A += ((e[0].x + e[1].x) + (e[2].x + e[3].x)) + ((e[4].x + e[5].x) + (e[6].x + e[7].x));
-  B += ((e[0].y + e[1].y) + (e[2].y + e[3].y)) + ((e[4].y + e[5].y) + (e[6].y + e[7].y));
+// (byte 3 of x) << 2, one VALU op (sub-dword operand select).
+__device__ __forceinline__ uint32_t byte3_x4(uint32_t x) {
+  uint32_t r;
+  asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3"
+      : "=v"(r) : "v"(x));
+  return r;
 }
 
+// Score terms of key word W (dimensions 8W..8W+7) from the LDS tables
+//   ta[P][f] = q^_{2P} c_K[f & 7] + q^_{2P+1} c_K[f >> 3]   (P: dimension pair)
+//   tb[W][s] = sum_j (bit j of s ? u : -u)_{8W+j}            (s: the word's sign byte)
+// The four 6-bit index pairs sit at bits 0, 6, 12 and 18 of the word: each is
+// brought to bits 2..7 of a byte (4 x index: a float offset) by a shift and
+// a byte-selecting AND; the sign byte by one byte-selecting shift.
+template <int W>
+__device__ __forceinline__ void key_word_score(const float* ta, const float* tb, uint32_t x,
+                                               float& A, float& B) {
+  const uint32_t m = 0xFCu;
+  const uint32_t f0 = and_byte<0>(m, x << 2);    // bits 0..5   -> byte 0 bits 2..7
+  const uint32_t f1 = and_byte<1>(m, x << 4);    // bits 6..11  -> byte 1 bits 2..7
+  const uint32_t f2 = and_byte<1>(m, x >> 2);    // bits 12..17 -> byte 1 bits 2..7
+  const uint32_t f3 = and_byte<2>(m, x);         // bits 18..23 -> byte 2 bits 2..7
+  const uint32_t fs = byte3_x4(x);               // sign byte, times 4
+  const char* pa = reinterpret_cast<const char*>(ta + (4 * W) * 64);
+  const char* pb = reinterpret_cast<const char*>(tb + W * 256);
+  const float a0 = *reinterpret_cast<const float*>(pa + f0);
+  const float a1 = *reinterpret_cast<const float*>(pa + 256 + f1);
+  const float a2 = *reinterpret_cast<const float*>(pa + 512 + f2);
+  const float a3 = *reinterpret_cast<const float*>(pa + 768 + f3);
+  const float b0 = *reinterpret_cast<const float*>(pb + fs);
+  A += (a0 + a1) + (a2 + a3);
+  B += b0;
+}
+
+
+
+// Token weights of a 64-token tile for the lane-per-dimension value loop.
+// Lane t holds w_t; two lane swaps give four registers R_j holding tokens
+// 16j .. 16j+15 in every 16-lane row (v_permlane32_swap exchanges the upper
+// half of one register with the lower half of another, v_permlane16_swap the
+// odd rows of one with the even rows of another). An FMA then reads w_{16j+k}
+// through a DPP row broadcast of lane k (row_newbcast), so no weight costs an
+// instruction of its own.
+struct TileWeights {
+  float r[4];
+};
+
+__device__ __forceinline__ TileWeights spread_weights(float w) {
+  const int wi = __float_as_int(w);
+  const auto h = __builtin_amdgcn_permlane32_swap(wi, wi, false, false);   // rows 0 1 0 1 | 2 3 2 3
+  const auto lo = __builtin_amdgcn_permlane16_swap(h[0], h[0], false, false);   // 0 0 0 0 | 1 1 1 1
+  const auto hi = __builtin_amdgcn_permlane16_swap(h[1], h[1], false, false);   // 2 2 2 2 | 3 3 3 3
+  TileWeights tw;
+  tw.r[0] = __int_as_float(lo[0]);
+  tw.r[1] = __int_as_float(lo[1]);
+  tw.r[2] = __int_as_float(hi[0]);
+  tw.r[3] = __int_as_float(hi[1]);
+  return tw;
+}
+
+// acc += w_{16j+K} * c, the weight taken from register R_j by a row broadcast.
+template <int K>
+__device__ __forceinline__ void fma_row_bcast(float& acc, float rj, float c) {
+  asm("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+      : "+v"(acc) : "v"(rj), "v"(c), "i"(K));
+}
+
+// The 16 tokens 8*W8 .. 8*W8+15 of two value words: acc_{jj & 3} += w_t c_V[code].
+// The 16 table reads are issued together (the empty asm makes them complete
+// before the first FMA), so the LDS latency is paid once per word pair.
+template <int W8>
+__device__ __forceinline__ void value_words(const TileWeights& tw, uint32_t x0, uint32_t x1,
+                                            const char* vtab, float& o0, float& o1, float& o2,
+                                            float& o3) {
+  uint32_t off[16];
+  nibble_offsets4(x0, *reinterpret_cast<uint32_t(*)[8]>(off));
+  nibble_offsets4(x1, *reinterpret_cast<uint32_t(*)[8]>(off + 8));
+  float c[16];
+#pragma unroll
+  for (int jj = 0; jj < 16; ++jj) c[jj] = *reinterpret_cast<const float*>(vtab + off[jj]);
+  asm volatile("" : "+v"(c[0]), "+v"(c[1]), "+v"(c[2]), "+v"(c[3]), "+v"(c[4]), "+v"(c[5]),
+               "+v"(c[6]), "+v"(c[7]), "+v"(c[8]), "+v"(c[9]), "+v"(c[10]), "+v"(c[11]),
+               "+v"(c[12]), "+v"(c[13]), "+v"(c[14]), "+v"(c[15]));
+  constexpr int J = W8 / 2;          // W8 is even: both words share R_J
+  const float rj = tw.r[J];
+  fma_row_bcast<0>(o0, rj, c[0]);
+  fma_row_bcast<1>(o1, rj, c[1]);
+  fma_row_bcast<2>(o2, rj, c[2]);
+  fma_row_bcast<3>(o3, rj, c[3]);
+  fma_row_bcast<4>(o0, rj, c[4]);
+  fma_row_bcast<5>(o1, rj, c[5]);
+  fma_row_bcast<6>(o2, rj, c[6]);
+  fma_row_bcast<7>(o3, rj, c[7]);
+  fma_row_bcast<8>(o0, rj, c[8]);
+  fma_row_bcast<9>(o1, rj, c[9]);
+  fma_row_bcast<10>(o2, rj, c[10]);
+  fma_row_bcast<11>(o3, rj, c[11]);
+  fma_row_bcast<12>(o0, rj, c[12]);
+  fma_row_bcast<13>(o1, rj, c[13]);
+  fma_row_bcast<14>(o2, rj, c[14]);
+  fma_row_bcast<15>(o3, rj, c[15]);
+}
+
+// The V residual term of one word: acc += sum_t (+-1 by the sign bit) g_t.
+template <int W8>
+__device__ __forceinline__ void value_sign_word(const TileWeights& tg, uint32_t x, float& acc) {
+  constexpr int J = W8 / 2, K0 = 8 * (W8 & 1);
+  const float rj = tg.r[J];
+  float sgn[8];
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) sgn[jj] = ((x >> (4 * jj + 3)) & 1u) ? 1.0f : -1.0f;
+  fma_row_bcast<K0 + 0>(acc, rj, sgn[0]);
+  fma_row_bcast<K0 + 1>(acc, rj, sgn[1]);
+  fma_row_bcast<K0 + 2>(acc, rj, sgn[2]);
+  fma_row_bcast<K0 + 3>(acc, rj, sgn[3]);
+  fma_row_bcast<K0 + 4>(acc, rj, sgn[4]);
+  fma_row_bcast<K0 + 5>(acc, rj, sgn[5]);
+  fma_row_bcast<K0 + 6>(acc, rj, sgn[6]);
+  fma_row_bcast<K0 + 7>(acc, rj, sgn[7]);
+}
 
 // N consecutive elements of an fp16 or fp32 vector, in two steps so that all
 // prologue loads are in flight before the first wait: load_raw issues the
@@ -311,12 +407,14 @@ template <int WAVES, bool VQJL>
 __global__ __launch_bounds__(WAVES * 64)
 __attribute__((amdgpu_waves_per_eu((WAVES == 8 && !VQJL) ? 6 : 1)))
 void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
-  constexpr int NPL = 16 / WAVES;          // table entries per lane and row
+  constexpr int TAM = 2048 / (WAVES * 64);   // pair-table entries per thread
+  constexpr int TBM = 512 / (WAVES * 64);    // groups of 4 sign-table entries per thread
   constexpr int COLS = kDim / WAVES;       // rows of Pi per thread in the epilogue
   constexpr int DEPTH = (WAVES == 8) ? 1 : 2;
   constexpr int NT = WAVES * 64;
   constexpr int PIV = 1024 / NT;          // float4 of Pi per thread
-  __shared__ float2 s_ktab[kDim * 16];
+  __shared__ float s_ta[32 * 64];          // pair table of the score's table term
+  __shared__ __attribute__((aligned(16))) float s_tb[8 * 256];   // sign-byte table of the QJL term
   __shared__ __attribute__((aligned(16))) float s_pi[kDim * kDim];
   __shared__ float s_vtab[16];
   __shared__ float s_part[WAVES][kDim];
@@ -355,13 +453,24 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   const bool paper = (a.flags & kQjlPaper) != 0;
 
   // ------------------------------------------- loads, in the order they are needed
-  const int row = t / WAVES, sub = t % WAVES;
+  // Table entries built by this thread (NT threads):
+  //   ta (2048 entries): e = t + NT m, pair P = e / 64, index f = e % 64 = t % 64
+  //   tb (2048 entries in groups of 4): group e = t + NT m of word w = e / 64,
+  //      sign bytes 4 (e % 64) .. 4 (e % 64) + 3
   const float* qu = a.qu + (int64_t)unit * 2 * kDim;
-  const float qh_row = qu[row];
-  const float u_row = qu[kDim + row];
-  float ck[NPL];
+  const int f_ta = t & 63;
+  const float ck_lo = a.lut_k[lh * 8 + (f_ta & 7)];
+  const float ck_hi = a.lut_k[lh * 8 + (f_ta >> 3)];
+  float2 qpair[TAM];
 #pragma unroll
-  for (int e = 0; e < NPL; ++e) ck[e] = a.lut_k[lh * 8 + ((sub * NPL + e) & 7)];
+  for (int m = 0; m < TAM; ++m) qpair[m] = reinterpret_cast<const float2*>(qu)[(t >> 6) + (NT / 64) * m];
+  float4 ulo[TBM], uhi[TBM];
+#pragma unroll
+  for (int m = 0; m < TBM; ++m) {
+    const int w = (t + NT * m) >> 6;
+    ulo[m] = reinterpret_cast<const float4*>(qu + kDim)[2 * w];
+    uhi[m] = reinterpret_cast<const float4*>(qu + kDim)[2 * w + 1];
+  }
   const float cv = a.lut_v[lh * 8 + (t & 7)];
   // (every prologue load is unconditional: a load under a branch makes the
   // compiler's wait counts after the join conservative)
@@ -380,9 +489,21 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   }
   // --------------------------------------------------------------- prologue
 #pragma unroll
-  for (int e = 0; e < NPL; ++e) {
-    const int nib = sub * NPL + e;
-    s_ktab[row * 16 + nib] = make_float2(qh_row * ck[e], (nib & 8) ? u_row : -u_row);
+  for (int m = 0; m < TAM; ++m)
+    s_ta[t + NT * m] = fmaf(qpair[m].y, ck_hi, qpair[m].x * ck_lo);
+#pragma unroll
+  for (int m = 0; m < TBM; ++m) {
+    const int e = t + NT * m, k = e & 63;
+    const float u[8] = {ulo[m].x, ulo[m].y, ulo[m].z, ulo[m].w, uhi[m].x, uhi[m].y, uhi[m].z, uhi[m].w};
+    float base = 0.0f;                 // sign bits 2..7 of the bytes 4k .. 4k+3 are the bits of k
+#pragma unroll
+    for (int j = 2; j < 8; ++j) base += ((k >> (j - 2)) & 1) ? u[j] : -u[j];
+    float4 v;
+    v.x = (base - u[0]) - u[1];
+    v.y = (base + u[0]) - u[1];
+    v.z = (base - u[0]) + u[1];
+    v.w = (base + u[0]) + u[1];
+    reinterpret_cast<float4*>(s_tb)[e] = v;
   }
   s_vtab[t & 15] = cv;             // every thread: identical values, no branch around the load
   lds_barrier();
@@ -406,7 +527,6 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   float sg = 0.0f;
   float o0 = 0.0f, o1 = 0.0f, o2 = 0.0f, o3 = 0.0f;
   const float lscale = a.logit_scale2;
-  const float2* ktab = s_ktab;
   const char* vtab = reinterpret_cast<const char*>(s_vtab);
 
   for (int tb = tile_begin + wave; tb < tile_end; tb += DEPTH * WAVES) {
@@ -417,21 +537,20 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
       const TileRegs& cur = buf[d];
       const int tok = tt * kTile + lane;
       const bool tv = tok < n;
-      // ---- key score, one lane per token. Two words (16 table reads) in
-      // flight at a time: the empty asm pins the partial sums so the compiler
-      // does not hoist every table read of the tile (registers, occupancy).
+      // ---- key score, one lane per token: per key word 4 pair-table reads
+      // (table term) and 1 sign-table read (QJL term). The empty asm pins the
+      // partial sums half way so the compiler does not hoist every table read
+      // of the tile (registers, occupancy).
       float A = 0.0f, B = 0.0f;
-      score_word(ktab + 0 * 128, cur.k0.x, A, B);
-      score_word(ktab + 1 * 128, cur.k0.y, A, B);
+      key_word_score<0>(s_ta, s_tb, cur.k0.x, A, B);
+      key_word_score<1>(s_ta, s_tb, cur.k0.y, A, B);
+      key_word_score<2>(s_ta, s_tb, cur.k0.z, A, B);
+      key_word_score<3>(s_ta, s_tb, cur.k0.w, A, B);
       asm volatile("" : "+v"(A), "+v"(B));
-      score_word(ktab + 2 * 128, cur.k0.z, A, B);
-      score_word(ktab + 3 * 128, cur.k0.w, A, B);
-      asm volatile("" : "+v"(A), "+v"(B));
-      score_word(ktab + 4 * 128, cur.k1.x, A, B);
-      score_word(ktab + 5 * 128, cur.k1.y, A, B);
-      asm volatile("" : "+v"(A), "+v"(B));
-      score_word(ktab + 6 * 128, cur.k1.z, A, B);
-      score_word(ktab + 7 * 128, cur.k1.w, A, B);
+      key_word_score<4>(s_ta, s_tb, cur.k1.x, A, B);
+      key_word_score<5>(s_ta, s_tb, cur.k1.y, A, B);
+      key_word_score<6>(s_ta, s_tb, cur.k1.z, A, B);
+      key_word_score<7>(s_ta, s_tb, cur.k1.w, A, B);
       const float nk = half_bits_to_float(cur.sc.x), gk = half_bits_to_float(cur.sc.x >> 16);
       const float nv = half_bits_to_float(cur.sc.y), gv = half_bits_to_float(cur.sc.y >> 16);
       const float coef = paper ? ebar_k : kQjlAlpha * gk;
@@ -452,41 +571,25 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
       const float wv = tv ? p * nv * 0.125f : 0.0f;
       const float wg = VQJL ? (paper ? wv : wv * gv) : 0.0f;
 
-      // ---- value accumulate, one lane per dimension; token weights from
-      // their lanes through scalar registers
+      // ---- value accumulate, one lane per dimension; token weights through
+      // row broadcasts (spread_weights)
       const uint32_t vw[8] = {cur.v0.x, cur.v0.y, cur.v0.z, cur.v0.w, cur.v1.x, cur.v1.y, cur.v1.z, cur.v1.w};
-      const int wvi = __float_as_int(wv);
-  #pragma unroll
-      for (int w8 = 0; w8 < 8; ++w8) {
-        const uint32_t x = vw[w8];
-        uint32_t off[8];
-        nibble_offsets4(x, off);     // (nibble & 7) * 4: float entries
-        float ws[8];
-  #pragma unroll
-        for (int jj = 0; jj < 8; ++jj) ws[jj] = __int_as_float(__builtin_amdgcn_readlane(wvi, 8 * w8 + jj));
-        o0 = fmaf(ws[0], *reinterpret_cast<const float*>(vtab + off[0]), o0);
-        o1 = fmaf(ws[1], *reinterpret_cast<const float*>(vtab + off[1]), o1);
-        o2 = fmaf(ws[2], *reinterpret_cast<const float*>(vtab + off[2]), o2);
-        o3 = fmaf(ws[3], *reinterpret_cast<const float*>(vtab + off[3]), o3);
-        o0 = fmaf(ws[4], *reinterpret_cast<const float*>(vtab + off[4]), o0);
-        o1 = fmaf(ws[5], *reinterpret_cast<const float*>(vtab + off[5]), o1);
-        o2 = fmaf(ws[6], *reinterpret_cast<const float*>(vtab + off[6]), o2);
-        o3 = fmaf(ws[7], *reinterpret_cast<const float*>(vtab + off[7]), o3);
-        if (w8 & 1) asm volatile("" : "+v"(o0), "+v"(o1), "+v"(o2), "+v"(o3));
-      }
+      const TileWeights tw = spread_weights(wv);
+      value_words<0>(tw, vw[0], vw[1], vtab, o0, o1, o2, o3);
+      value_words<2>(tw, vw[2], vw[3], vtab, o0, o1, o2, o3);
+      value_words<4>(tw, vw[4], vw[5], vtab, o0, o1, o2, o3);
+      value_words<6>(tw, vw[6], vw[7], vtab, o0, o1, o2, o3);
       if (VQJL) {
-        const int wgi = __float_as_int(wg);
-  #pragma unroll
-        for (int w8 = 0; w8 < 8; ++w8) {
-          const uint32_t x = vw[w8];
-  #pragma unroll
-          for (int jj = 0; jj < 8; ++jj) {
-            const float g = __int_as_float(__builtin_amdgcn_readlane(wgi, 8 * w8 + jj));
-            sg += ((x >> (4 * jj + 3)) & 1u) ? g : -g;
-          }
-        }
+        const TileWeights tg = spread_weights(wg);
+        value_sign_word<0>(tg, vw[0], sg);
+        value_sign_word<1>(tg, vw[1], sg);
+        value_sign_word<2>(tg, vw[2], sg);
+        value_sign_word<3>(tg, vw[3], sg);
+        value_sign_word<4>(tg, vw[4], sg);
+        value_sign_word<5>(tg, vw[5], sg);
+        value_sign_word<6>(tg, vw[6], sg);
+        value_sign_word<7>(tg, vw[7], sg);
       }
-
         const int tn = tt + DEPTH * WAVES;
         if (tn < tile_end) load_tile(buf[d], kreg, vreg, sreg, tile0 + tn, s0, tn, lane);
     }

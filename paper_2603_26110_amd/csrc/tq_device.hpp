@@ -3,11 +3,13 @@
 // Cache layout (64-slot tiles, 2048 bytes per tile per tensor):
 //   K tile, token-major: 16-byte half c (codes 32c..32c+31) of slot-in-tile r
 //        at byte (c*64 + r)*16. One lane per token loads its 32 bytes with two
-//        128-bit loads; each wave-wide load covers 1 KiB contiguously.
+//        128-bit loads; each wave-wide load covers 1 KiB contiguously. Key word
+//        w holds dimensions 8w..8w+7: 3-bit index of dimension 8w+j in bits
+//        3j..3j+2, its QJL sign bit in bit 24+j.
 //   V tile, dimension-major: 16-byte half c (slots 32c..32c+31) of dimension i
 //        at byte (c*64 + i)*16. One lane per dimension loads the 64 codes of its
-//        dimension for the whole tile with two 128-bit loads.
-//   A nibble is idx | sign << 3; nibble j of a 32-bit word sits at bits 4j..4j+3.
+//        dimension for the whole tile with two 128-bit loads. A value nibble is
+//        idx | sign << 3; nibble j of a 32-bit word sits at bits 4j..4j+3.
 //   Scalars: 4 x fp16 per slot [n_k, g_k, n_v, g_v] at byte slot*8.
 #pragma once
 
@@ -48,6 +50,13 @@ __device__ __forceinline__ float half_bits_to_float(uint32_t bits) {
   return __half2float(__ushort_as_half((unsigned short)(bits & 0xFFFFu)));
 }
 
+// Key word of dimensions 8w..8w+7: 3-bit index of dimension 8w+j in bits
+// 3j..3j+2, its QJL sign bit in bit 24+j. Value words hold eight 4-bit
+// nibbles idx | sign << 3.
+__device__ __forceinline__ uint32_t key_code_bits(uint32_t idx, uint32_t sign, int j) {
+  return (idx << (3 * j)) | (sign << (24 + j));
+}
+
 // Byte offset of 16-byte half c of row r (slot for K, dimension for V) in a tile.
 __device__ __forceinline__ int64_t tile_half_offset(int64_t tile, int c, int r) {
   return tile * kTileBytes + (int64_t)(c * kTile + r) * 16;
@@ -63,7 +72,9 @@ __device__ __forceinline__ int64_t tile_half_offset(int64_t tile, int c, int r) 
 //   L        ascending table and its midpoints (0.5f * (c_m + c_{m+1}))
 //   S        64 x 64 projection in LDS (row-major); unused unless sign_mode == 1
 //   sign_mode 0 none, 1 projected (S r), 2 per element (r)
-//   words[8] out: nibble words (idx | sign << 3)
+//   words[8] out: with KEY_WORDS the key word format (index of dimension 8w+j
+//            in bits 3j..3j+2, its sign in bit 24+j), else nibble words
+//            (idx | sign << 3 in bits 4j..4j+3)
 // The eight levels and seven midpoints of one table as named register values.
 // Named members (no arrays) keep the level choice a chain of selects between
 // registers; an array indexed inside a loop gets folded into an indexed load
@@ -117,6 +128,7 @@ struct QuantOut {
   uint32_t n16, g16;
 };
 
+template <bool KEY_WORDS>
 __device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Levels& L,
                                                   const float* S, int sign_mode,
                                                   uint32_t (&words)[8]) {
@@ -133,7 +145,7 @@ __device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Level
     const float u = xh[i] * inv;
     uint32_t idx;
     const float lv = nearest_level(u, TQ_LEVELS(L), &idx);
-    words[i >> 3] |= idx << (4 * (i & 7));
+    words[i >> 3] |= idx << ((KEY_WORDS ? 3 : 4) * (i & 7));
     xh[i] = u - lv;   // residual r_i
   }
   float gs = 0.0f;
@@ -161,7 +173,7 @@ __device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Level
   }
 #pragma unroll
   for (int i = 0; i < kDim; ++i)
-    words[i >> 3] |= (uint32_t)((sbits >> i) & 1u) << (4 * (i & 7) + 3);
+    words[i >> 3] |= (uint32_t)((sbits >> i) & 1u) << (KEY_WORDS ? 24 + (i & 7) : 4 * (i & 7) + 3);
   QuantOut o;
   o.n16 = store_norm(n);
   o.g16 = (sign_mode == 0) ? 0u : store_norm(g);

@@ -149,7 +149,7 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
     rotate_lane(x, s_pi, s_col, lane);
   }
   uint32_t kw[8];
-  const QuantOut qk = quantize_lane(x, Lk, s_S, ksign, kw);
+  const QuantOut qk = quantize_lane<true>(x, Lk, s_S, ksign, kw);
   if (ok) {
     const int64_t tile = slot >> 6;
     const int r = (int)(slot & 63);
@@ -162,7 +162,7 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
   for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.v, row + i, F16) : 0.0f;
   if (!rotated && (a.flags & kVRotate)) rotate_lane(x, s_pi, s_col, lane);
   uint32_t vw[8];
-  const QuantOut qv = quantize_lane(x, Lv, s_S, vsign, vw);
+  const QuantOut qv = quantize_lane<false>(x, Lv, s_S, vsign, vw);
   if (ok) {
     *reinterpret_cast<uint2*>(a.scalars + (lh * a.slots + slot) * 4) =
         make_uint2(qk.n16 | (qk.g16 << 16), qv.n16 | (qv.g16 << 16));
@@ -375,8 +375,9 @@ __global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, uint
   const int64_t tile = slot >> 6;
   const int r = (int)(slot & 63);
   if (!is_v) {
-    // key: token-major, 8 nibbles per 32-bit word; lane 8w ends with word w
-    uint32_t word = nib << (4 * (i & 7));
+    // key: token-major key words (index bits 3j, sign bit 24 + j); lane 8w
+    // ends with word w
+    uint32_t word = key_code_bits(nib & 7u, nib >> 3, i & 7);
     word |= __shfl_xor(word, 1, 64);
     word |= __shfl_xor(word, 2, 64);
     word |= __shfl_xor(word, 4, 64);

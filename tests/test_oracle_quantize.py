@@ -154,34 +154,44 @@ def test_brute_force_index_on_small_grid():
 
 # ------------------------------------------------------------------ packing
 def test_pack_layout_hand_worked():
-    # Slot 65 = tile 1, lane 1. Nibble 9 = word 1, bits 4..7. Word 1 is in the
-    # first 16-byte half, bytes 4..7 of it; that half sits at
-    # 1*2048 + (0*64 + 1)*16 = 2064. So byte 2064 + 4 + 0 holds 0xA0.
+    # Slot 65 = tile 1, lane 1. Code 9 = word 1, position j = 1: index bits
+    # 3..5, sign bit 25. Word 1 is in the first 16-byte half, bytes 4..7 of
+    # it; that half sits at 1*2048 + (0*64 + 1)*16 = 2064.
     region = np.zeros(4096, np.uint8)
     nib = np.zeros(64, np.uint8)
-    nib[9] = 0xA
+    nib[9] = 0x5                      # index 5, sign 0 -> 0b101 << 3 = 0x28
     oracle.pack_slot(region, 65, nib)
-    assert np.flatnonzero(region).tolist() == [2068] and region[2068] == 0xA0
-    # Nibble 63 = word 7 (second half, bytes 12..15), bits 28..31 -> byte 15
-    # of the half at 2048 + (64 + 1)*16 = 3088.
+    assert np.flatnonzero(region).tolist() == [2068] and region[2068] == 0x28
+    nib[9] = 0xD                      # index 5, sign 1 -> also bit 25 = bit 1 of byte 3
+    region[:] = 0
+    oracle.pack_slot(region, 65, nib)
+    assert np.flatnonzero(region).tolist() == [2068, 2071]
+    assert region[2068] == 0x28 and region[2071] == 0x02
+    # Code 63 = word 7 (second half, bytes 12..15), j = 7: index bits 21..23
+    # (top of byte 2), sign bit 31 (top of byte 3); the half is at
+    # 2048 + (64 + 1)*16 = 3088.
     region[:] = 0
     nib[:] = 0
-    nib[63] = 0x7
+    nib[63] = 0xF
     oracle.pack_slot(region, 65, nib)
-    assert np.flatnonzero(region).tolist() == [3088 + 15] and region[3103] == 0x70
+    assert np.flatnonzero(region).tolist() == [3088 + 14, 3088 + 15]
+    assert region[3102] == 0xE0 and region[3103] == 0x80
 
 
 def test_pack_matches_vectorized_shift_sum_and_round_trips():
-    # Independent construction: 8 nibbles per 32-bit word by a broadcast shift
-    # and sum (the vectorized packing of Sec. 4.2 with 4-bit fields), then
-    # placement of the two 16-byte halves.
+    # Independent construction: per 32-bit word, the 3-bit indices by a
+    # broadcast shift and sum at 3j (the vectorized packing of Sec. 4.2 with
+    # 3-bit fields) plus the sign bits at 24 + j, then placement of the two
+    # 16-byte halves.
     g = synth.rng(6)
     slots = 256
     region = np.zeros(slots * 32, np.uint8)
     allnib = g.integers(0, 16, (slots, 64)).astype(np.uint8)
     for s in range(slots):
         oracle.pack_slot(region, s, allnib[s])
-    words = (allnib.reshape(slots, 8, 8).astype(np.uint32) << (4 * np.arange(8, dtype=np.uint32))).sum(-1)
+    n8 = allnib.reshape(slots, 8, 8).astype(np.uint32)
+    j = np.arange(8, dtype=np.uint32)
+    words = ((n8 & 7) << (3 * j)).sum(-1) + (((n8 >> 3) & 1) << (24 + j)).sum(-1)
     wbytes = words.astype("<u4").view(np.uint8).reshape(slots, 2, 16)
     ref = np.zeros(slots * 32, np.uint8)
     for s in range(slots):
