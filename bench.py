@@ -1,13 +1,16 @@
-"""Benchmark: fused 3-bit decode attention on the full ESM-2 650M cache shape.
+"""Benchmark: one decode step of TurboESM on the full ESM-2 650M cache shape.
 
 Workload (default "esm2-650m-33layer-seq1024"): 33 layers x 20 heads x 64,
 batch 1, 1024 cached tokens, fp16 I/O, synthetic seeded inputs. One step =
-quantize_pack of the new token for all 33 layers (RoPE, rotation, 3-bit codes,
-QJL signs, packing) + decode_attend over the 1025 cached tokens of all 33
-layers (one launch each). Steps rotate over replicas of every per-step input
-(cache, Pi, query, new token) totalling >= 1 GiB, so each step reads its data
-from HBM rather than from the 256 MB Infinity Cache. The K timed steps are
-captured in one HIP graph and replayed once between two synchronizations.
+tq_decode_step over all 33 layers: append the new token (RoPE, rotation,
+3-bit codes, QJL signs, packing) and attend over the 1025 cached tokens, as
+two kernel launches (a step prologue that rotates the query and quantizes
+the new key and value with one read of each Pi, then the attention kernel).
+Steps rotate over replicas of every per-step input (cache, Pi, query, new
+token) totalling >= 1 GiB, so each step reads its data from HBM rather than
+from the 256 MB Infinity Cache. The K timed steps are captured in one HIP
+graph and replayed once between two synchronizations; HIP events on the
+graph's stream give the average step duration for the roofline.
 
 Prints one JSON line (see the "value", "roofline" and "cpu_baseline" keys).
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
@@ -100,6 +103,7 @@ def main():
     zero_i32, zero_i64 = t_(np.zeros(1, np.int32)), t_(np.zeros(1, np.int64))
     pos_new, slot_new = t_(np.array([T], np.int32)), t_(np.array([T], np.int64))
     qpos, slen = t_(np.array([n_ctx - 1], np.int32)), t_(np.array([n_ctx], np.int32))
+    cached = t_(np.array([T], np.int32))           # tokens in the cache before a step
 
     # replica 0: prefill the cache with the first T tokens
     base_cache = tq.Cache(L, H, slots, device=dev)
@@ -117,7 +121,8 @@ def main():
         c.k_codes.copy_(base_cache.k_codes)
         c.v_codes.copy_(base_cache.v_codes)
         c.scalars.copy_(base_cache.scalars)
-        reps.append(dict(cache=c, pi=pi_d.clone(), q=q_d.clone(), k=k_new.clone(), v=v_new.clone(),
+        kr, vr = k_new.clone(), v_new.clone()
+        reps.append(dict(cache=c, pi=pi_d.clone(), q=q_d.clone(), k=kr, v=vr, k1=kr[:, :, 0], v1=vr[:, :, 0],
                          out=torch.empty_like(q_d)))
     ws_bytes = tq.decode_workspace_bytes(params, 1, L, n_ctx)
     ws = torch.zeros(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
@@ -133,14 +138,26 @@ def main():
                          S_d, out=d["out"], workspace=ws)
 
     def step(r):
+        # append the token at position T (slot T) and attend over T + 1 tokens
+        d = reps[r]
+        tq.decode_step(params, d["cache"], d["q"], d["k1"], d["v1"], pos_new, zero_i64, cached, n_ctx,
+                       d["pi"], lut_d, lut_d, S_d, out=d["out"], workspace=ws)
+
+    def two_calls(r):
         append(r)
         attend(r)
 
     # warmup (eager), then check that a graph replay reproduces the eager output
+    # and that the fused step gives what the two separate calls give
+    for s in range(args.warmup):
+        two_calls(s % R)
+    torch.cuda.synchronize()
+    two_call_out = reps[0]["out"].clone()
     for s in range(args.warmup):
         step(s % R)
     torch.cuda.synchronize()
     eager_out = reps[0]["out"].clone()
+    assert torch.equal(eager_out, two_call_out), "decode_step differs from quantize_pack + decode_attend"
 
     K = args.steps
     if args.eager:
@@ -150,43 +167,61 @@ def main():
         print(json.dumps({"eager_steps": K, "decode_only": bool(args.decode_only)}))
         return
     stream = torch.cuda.Stream(device=dev)
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph, stream=stream):
-        for s in range(K):
-            (attend if args.decode_only else step)(s % R)
-    graph.replay()                                  # untimed warm replay
-    torch.cuda.synchronize()
-    assert torch.equal(reps[0]["out"], eager_out), "graph replay differs from eager decode"
 
-    # timed region: exactly K steps
+    def capture(fn):
+        g_ = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_, stream=stream):
+            for s in range(K):
+                fn(s % R)
+        g_.replay()                                 # untimed warm replay
+        torch.cuda.synchronize()
+        return g_
+
+    graph = capture(attend if args.decode_only else step)
+    if not args.decode_only:
+        assert torch.equal(reps[0]["out"], eager_out), "graph replay differs from eager decode"
+
+    # timed region: exactly K steps; HIP events on the graph's stream give the
+    # average step duration for the roofline
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    graph.replay()
+    with torch.cuda.stream(stream):
+        e0.record(stream)
+        graph.replay()
+        e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / K
+    step_ms = e0.elapsed_time(e1) / K
 
-    # decode-only graph, timed with HIP events on its stream: average launch duration
-    dgraph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(dgraph, stream=stream):
-        for s in range(K):
-            attend(s % R)
-    dgraph.replay()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    with torch.cuda.stream(stream):
-        e0.record(stream)
-        dgraph.replay()
-        e1.record(stream)
-    torch.cuda.synchronize()
-    decode_ms = e0.elapsed_time(e1) / K
+    # for comparison (not the headline): the same step as two calls, and the
+    # attention call alone
+    def graph_ms(fn):
+        g_ = capture(fn)
+        a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            a_.record(stream)
+            g_.replay()
+            b_.record(stream)
+        torch.cuda.synchronize()
+        return a_.elapsed_time(b_) / K
+
+    two_call_ms = graph_ms(two_calls) if not args.decode_only else None
+    attend_ms = graph_ms(attend) if not args.decode_only else step_ms
 
     units = L * H
     kv_bytes = units * n_ctx * 72
     pi_bytes = units * 64 * 64 * 4
     io_b = 2 if io == torch.float16 else 4
-    alg_bytes = kv_bytes + pi_bytes + units * 64 * io_b * 2 + units * 8 * 4 * 2 + 64 * 64 * 4
-    achieved = alg_bytes / (decode_ms * 1e-3) / 1e9
+    # algorithmic bytes of one step: every cached token-head once (72 B), each
+    # Pi once, S and the tables once, q, k, v in and out once, and the new
+    # token-head written (72 B)
+    alg_bytes = (kv_bytes + pi_bytes + 64 * 64 * 4 + units * 8 * 4 * 2 + units * 64 * io_b * 4
+                 + units * 72)
+    if args.decode_only:
+        alg_bytes = kv_bytes + pi_bytes + 64 * 64 * 4 + units * 8 * 4 * 2 + units * 64 * io_b * 2
+    achieved = alg_bytes / (step_ms * 1e-3) / 1e9
     value = kv_bytes / (ms_per_step * 1e-3) / 1e9
 
     cpu = None
@@ -211,11 +246,14 @@ def main():
                    "replica_bytes": int(R * per_replica)},
         "kv_pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "decode_steps_per_s": round(1e3 / ms_per_step, 1),
-        "decode_kernel_ms": round(decode_ms, 5),
-        "decode_kv_gbs": round(kv_bytes / (decode_ms * 1e-3) / 1e9, 2),
+        "step_event_ms": round(step_ms, 5),
+        "two_call_step_ms": None if two_call_ms is None else round(two_call_ms, 5),
+        "decode_attend_ms": round(attend_ms, 5),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "decode_kernel", "alg_bytes_per_launch": int(alg_bytes)},
+                     "kernel": ("decode_attend: prep + attention kernels" if args.decode_only else
+                                "decode_step: step prologue + attention kernels"),
+                     "alg_bytes_per_launch": int(alg_bytes)},
         "cpu_baseline": cpu,
         "paper_context": {"memory_reduction": "7.1x (Table 4, fp32 baseline, 'CUDA')",
                           "kv_fetch_speedup": "1.96x Triton vs PyTorch fetch_unpacked, 143 tokens, "

@@ -24,10 +24,13 @@
  * as documented per entry point.
  *
  * Fixed layout facts (head_dim must be 64):
- *   - code words: a token-head vector of 64 codes is 32 bytes; code i is the
- *     nibble at bits 4*(i%8) .. 4*(i%8)+3 of 32-bit word i/8 (little endian).
- *     Nibble = idx | (sign << 3): idx is the 3-bit LUT index, sign the QJL bit
- *     (K always; V only with TQ_V_QJL, else 0).
+ *   - code words: a token-head vector of 64 codes is 32 bytes, eight 32-bit
+ *     little-endian words; word w covers dimensions 8w .. 8w+7. idx is the
+ *     3-bit LUT index of a dimension, sign its QJL bit.
+ *     Key word: idx of dimension 8w+j at bits 3j .. 3j+2 (bits 0-23), sign of
+ *       dimension 8w+j at bit 24+j (bits 24-31).
+ *     Value nibbles: dimension-major (below); a nibble is idx | (sign << 3),
+ *       sign = 0 unless TQ_V_QJL.
  *   - tiles: slots are grouped in tiles of 64; a tile holds 2048 bytes of
  *     k_codes and 2048 bytes of v_codes. Region (l, h) starts at byte
  *     (l*H + h)*slots*32 of each plane; slot s is in tile t = s/64 at r = s%64.
@@ -199,8 +202,40 @@ TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache
                            void* out, void* workspace, size_t workspace_bytes,
                            void* stream);
 
-/* Workspace bytes tq_decode_attend needs for these sizes (0 only for empty
- * or invalid sizes). */
+/* One decode step (Sec. 3.1 decode steps: quantize-then-attend): for every
+ * layer, sequence b and head, first append the new token exactly as
+ * tq_quantize_pack with T = 1, pos0 = pos and slot0 = seq_slot0 + seq_len
+ * would (same codes), then attend as tq_decode_attend with q_pos = pos and
+ * seq_len[b] + 1 cached tokens (same output). One kernel rotates the query
+ * and quantizes the new key and value of each (layer, sequence, head) with a
+ * single read of its Pi; the attention kernel follows.
+ *
+ *   q, k, v device [nlayers][B][H][64] io_dtype, before RoPE; 16-byte aligned.
+ *           k and v are the new token's key and value.
+ *   pos     device int32 [B]: RoPE position of the new token and of the query.
+ *   seq_slot0 device int64 [B]: first slot of each sequence, multiple of 64.
+ *   seq_len device int32 [B]: tokens cached BEFORE the step; the new token
+ *           goes to slot seq_slot0[b] + seq_len[b] and the step attends over
+ *           seq_len[b] + 1 tokens. The caller advances its own lengths.
+ *           A sequence that would exceed max_len, its slot range or the RoPE
+ *           table is not appended and gets NaN output.
+ *   max_len host bound on every seq_len[b] + 1, >= 1.
+ *   pi, lut_k, lut_v, qjl_s, ebar, out: as tq_decode_attend.
+ *   workspace as tq_decode_attend, >= tq_decode_workspace_bytes(params, B,
+ *           nlayers, max_len) bytes.
+ */
+TQ_API tq_status tq_decode_step(const tq_params* params, const tq_cache* cache,
+                         const void* q, const void* k, const void* v,
+                         int32_t B, int32_t layer0, int32_t nlayers,
+                         const int32_t* pos, const int64_t* seq_slot0,
+                         const int32_t* seq_len, int32_t max_len,
+                         const float* pi, const float* lut_k, const float* lut_v,
+                         const float* qjl_s, const float* ebar,
+                         void* out, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/* Workspace bytes tq_decode_attend and tq_decode_step need for these sizes
+ * (0 only for empty or invalid sizes). */
 TQ_API size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B,
                                  int32_t nlayers, int32_t max_len);
 

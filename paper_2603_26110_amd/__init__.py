@@ -6,8 +6,8 @@ path runs in the library's HIP kernels. If the library is not built, calls
 raise ``RuntimeError`` (there is no fallback path).
 
 Entry points (same names as the C ABI without the ``tq_`` prefix):
-    rope_table, quantize_pack, decode_attend, decode_workspace_bytes,
-    calibrate_rotation, cache_bytes, last_error, version
+    rope_table, quantize_pack, decode_attend, decode_step,
+    decode_workspace_bytes, calibrate_rotation, cache_bytes, last_error, version
 """
 from __future__ import annotations
 
@@ -18,7 +18,7 @@ from dataclasses import dataclass
 import torch
 
 __all__ = [
-    "Params", "Cache", "TQError", "rope_table", "quantize_pack", "decode_attend",
+    "Params", "Cache", "TQError", "rope_table", "quantize_pack", "decode_attend", "decode_step",
     "decode_workspace_bytes", "calibrate_rotation", "cache_bytes", "last_error", "version",
     "V_ROTATE", "V_QJL", "QJL_PAPER", "ROPE_HALF", "INPUT_ROTATED", "OUT_FP32", "lib_path",
 ]
@@ -68,6 +68,8 @@ def _load():
     L.tq_quantize_pack.restype = i32
     L.tq_decode_attend.argtypes = [P, P, P, i32, i32, i32, P, P, P, i32, P, P, P, P, P, P, P, sz, P]
     L.tq_decode_attend.restype = i32
+    L.tq_decode_step.argtypes = [P, P, P, P, P, i32, i32, i32, P, P, P, i32, P, P, P, P, P, P, P, sz, P]
+    L.tq_decode_step.restype = i32
     L.tq_decode_workspace_bytes.argtypes = [P, i32, i32, i32]
     L.tq_decode_workspace_bytes.restype = sz
     L.tq_calibrate_rotation.argtypes = [P, i32, i32, P, P, P]
@@ -212,6 +214,45 @@ def decode_attend(params: Params, cache: Cache, q, q_pos, seq_slot0, seq_len, ma
                               _ptr(seq_slot0), _ptr(seq_len), int(max_len), _ptr(pi), _ptr(lut_k),
                               _ptr(lut_v), _ptr(qjl_s), _ptr(ebar), _ptr(out), _ptr(workspace),
                               wsz, _stream(q.device)))
+    return out
+
+
+def decode_step(params: Params, cache: Cache, q, k, v, pos, seq_slot0, seq_len, max_len: int,
+                pi, lut_k, lut_v, qjl_s, ebar=None, layer0: int = 0, out=None,
+                workspace=None) -> torch.Tensor:
+    """Append the new token (k, v) and attend with q, all [nlayers][B][H][64].
+    seq_len holds the tokens cached before the step; the step attends over
+    seq_len + 1 of them. Returns out [nlayers][B][H][64]."""
+    L = _load()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        _dev(t, name, params.io_dtype)
+    if q.dim() != 4 or q.shape[-1] != 64 or q.shape[2] != params.num_heads:
+        raise ValueError("q must be [nlayers][B][H][64]")
+    if k.shape != q.shape or v.shape != q.shape:
+        raise ValueError("k and v must have the shape of q")
+    nl, B = q.shape[:2]
+    _dev(pos, "pos", torch.int32)
+    _dev(seq_slot0, "seq_slot0", torch.int64)
+    _dev(seq_len, "seq_len", torch.int32)
+    for name, t in (("pi", pi), ("lut_k", lut_k), ("lut_v", lut_v), ("qjl_s", qjl_s)):
+        _dev(t, name, torch.float32)
+    if ebar is not None:
+        _dev(ebar, "ebar", torch.float32)
+    out_dtype = torch.float32 if (params.flags & OUT_FP32 or params.io_dtype == torch.float32) \
+        else torch.float16
+    if out is None:
+        out = torch.empty(q.shape, dtype=out_dtype, device=q.device)
+    _dev(out, "out", out_dtype)
+    need = decode_workspace_bytes(params, B, nl, max_len)
+    if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.zeros(need, dtype=torch.uint8, device=q.device)
+    p = params.c()
+    c = cache.c()
+    wsz = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(L.tq_decode_step(ctypes.byref(p), ctypes.byref(c), _ptr(q), _ptr(k), _ptr(v), B, layer0, nl,
+                            _ptr(pos), _ptr(seq_slot0), _ptr(seq_len), int(max_len), _ptr(pi),
+                            _ptr(lut_k), _ptr(lut_v), _ptr(qjl_s), _ptr(ebar), _ptr(out),
+                            _ptr(workspace), wsz, _stream(q.device)))
     return out
 
 

@@ -133,24 +133,32 @@ size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B, int32_t nla
   return bytes;
 }
 
-tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const void* q, int32_t B,
-                           int32_t layer0, int32_t nlayers, const int32_t* q_pos,
-                           const int64_t* seq_slot0, const int32_t* seq_len, int32_t max_len,
-                           const float* pi, const float* lut_k, const float* lut_v,
-                           const float* qjl_s, const float* ebar, void* out, void* workspace,
-                           size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared by tq_decode_attend and tq_decode_step (k, v non-NULL: append first).
+tq_status decode_common(const tq_params* params, const tq_cache* cache, const void* q, const void* k,
+                        const void* v, int32_t B, int32_t layer0, int32_t nlayers, const int32_t* q_pos,
+                        const int64_t* seq_slot0, const int32_t* seq_len, int32_t max_len,
+                        const float* pi, const float* lut_k, const float* lut_v, const float* qjl_s,
+                        const float* ebar, void* out, void* workspace, size_t workspace_bytes,
+                        void* stream, bool step) {
   tq_status s = check_params(params, true);
   if (s != TQ_OK) return s;
   if ((s = check_cache(cache)) != TQ_OK) return s;
   if (params->flags & TQ_INPUT_ROTATED) return fail(TQ_ERR_ARG, "TQ_INPUT_ROTATED applies to tq_quantize_pack only");
   if (B < 0 || nlayers < 0 || max_len < 0) return fail(TQ_ERR_ARG, "B, nlayers and max_len must be >= 0");
+  if (step && max_len < 1) return fail(TQ_ERR_ARG, "a decode step attends to at least one token (max_len >= 1)");
   if (layer0 < 0 || layer0 + nlayers > params->num_layers)
     return fail(TQ_ERR_DIM, "layers [%d, %d) outside [0, %d)", layer0, layer0 + nlayers, params->num_layers);
   if ((int64_t)B * nlayers == 0) return ok();
   if (!q || !q_pos || !seq_slot0 || !seq_len || !pi || !lut_k || !lut_v || !qjl_s || !out)
     return fail(TQ_ERR_ARG, "a required pointer is NULL");
+  if (step && (!k || !v)) return fail(TQ_ERR_ARG, "k and v must not be NULL");
   if ((params->flags & TQ_QJL_PAPER) && !ebar) return fail(TQ_ERR_ARG, "TQ_QJL_PAPER needs ebar");
   if (!aligned(q, 16) || !aligned(out, 16)) return fail(TQ_ERR_ALIGN, "q and out must be 16-byte aligned");
+  if (step && (!aligned(k, 16) || !aligned(v, 16))) return fail(TQ_ERR_ALIGN, "k and v must be 16-byte aligned");
   if (!aligned(pi, 16) || !aligned(qjl_s, 16)) return fail(TQ_ERR_ALIGN, "pi and qjl_s must be 16-byte aligned");
   if ((int64_t)max_len > cache->slots) return fail(TQ_ERR_CAPACITY, "max_len exceeds the cache slots");
   const int64_t units = (int64_t)nlayers * B * params->num_heads;
@@ -179,6 +187,7 @@ tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const
   a.scalars = (const uint16_t*)cache->scalars; a.slots = cache->slots;
   a.out = out;
   a.nsplit = nsplit; a.split_tiles = split_tiles;
+  a.k_new = k; a.v_new = v; a.append = step ? 1 : 0; a.len_add = step ? 1 : 0;
   char* ws = (char*)workspace;
   a.qu = (float*)ws;
   ws += align256((size_t)units * 2 * 64 * sizeof(float));
@@ -187,7 +196,33 @@ tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const
     ws += align256((size_t)units * nsplit * tq::kPartialFloats * sizeof(float));
     a.counters = (uint32_t*)ws;
   }
-  return hip_status(tq::launch_decode(a, waves, (hipStream_t)stream), "tq_decode_attend launch");
+  return hip_status(tq::launch_decode(a, waves, (hipStream_t)stream),
+                    step ? "tq_decode_step launch" : "tq_decode_attend launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const void* q, int32_t B,
+                           int32_t layer0, int32_t nlayers, const int32_t* q_pos,
+                           const int64_t* seq_slot0, const int32_t* seq_len, int32_t max_len,
+                           const float* pi, const float* lut_k, const float* lut_v,
+                           const float* qjl_s, const float* ebar, void* out, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  return decode_common(params, cache, q, nullptr, nullptr, B, layer0, nlayers, q_pos, seq_slot0, seq_len,
+                       max_len, pi, lut_k, lut_v, qjl_s, ebar, out, workspace, workspace_bytes, stream,
+                       false);
+}
+
+tq_status tq_decode_step(const tq_params* params, const tq_cache* cache, const void* q, const void* k,
+                         const void* v, int32_t B, int32_t layer0, int32_t nlayers, const int32_t* pos,
+                         const int64_t* seq_slot0, const int32_t* seq_len, int32_t max_len,
+                         const float* pi, const float* lut_k, const float* lut_v, const float* qjl_s,
+                         const float* ebar, void* out, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  return decode_common(params, cache, q, k, v, B, layer0, nlayers, pos, seq_slot0, seq_len, max_len, pi,
+                       lut_k, lut_v, qjl_s, ebar, out, workspace, workspace_bytes, stream, true);
 }
 
 tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal, float* pi_out,

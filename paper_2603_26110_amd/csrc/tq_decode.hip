@@ -7,26 +7,32 @@
 //   inverse rotation of Algorithm 1 (identical by Eq. 4). Each row of Pi is
 //   shared by 4 contiguous lanes; a lane applies RoPE to its 16-element slice
 //   of q in registers and the lanes of a row combine their partial sums with
-//   DPP.
+//   DPP. For a decode step (APPEND) the same block first quantizes the new
+//   key and value into the cache (quantize-then-attend), reusing its read of
+//   Pi: the wave-per-vector quantizer of the append kernel, on Pi and S
+//   staged in LDS.
 //
 // decode_kernel (one block of WAVES waves per unit, or per split of its tiles)
 //   The cache read is bandwidth-bound and, with every block streaming at
-//   once, any load issued behind the stream waits for it. So nothing the
-//   block computes may wait on a load chained behind another: the 512 bytes of
-//   (q^, u) from the prep kernel are requested first, then every tile of the
-//   unit (two register buffers per wave and, for the first waves, one more
-//   tile loaded straight into LDS), then Pi for the epilogue straight into
-//   LDS. Per block:
-//   prologue  an LDS table T[i][nibble] = (q^_i c_K[nibble & 7], +-u_i), so one
-//             table read per code gives both score terms; one barrier.
-//   main loop keys are scored one lane per token:
-//             score = n_k/8 (sum_i T_A + coef sum_i T_B), coef = alpha g_k
-//             (QJL) or ebar_K. Online softmax in base 2 with a wave-uniform
-//             running max that is raised only when a tile max exceeds it by more
-//             than 2^8 (rescaling is rare). Values are accumulated one lane per
-//             dimension from the dimension-major V tile; the tile's token weights
-//             reach every lane through v_readlane (scalar registers), which
-//             keeps them off the LDS pipe that the table reads load.
+//   once, a load issued behind the stream waits for it. So the block's own
+//   small inputs (q^ and u, the two tables, the sequence's bounds) come
+//   through scalar loads, all issued together before anything else; the
+//   block's first tiles are requested after its tables are built, and Pi for
+//   the epilogue goes straight into LDS after the last prologue barrier.
+//   prologue  two LDS tables per unit: a pair table
+//               T_A[p][a + 8 b] = q^_{2p} c_K[a] + q^_{2p+1} c_K[b]
+//             (one read scores two dimensions' table terms) and a sign table
+//               T_B[w][s] = sum_j u_{8w+j} (2 s_j - 1)
+//             over the 8 sign bits s of key word w (one read per word for the
+//             QJL term).
+//   main loop keys are scored one lane per token from the key words (3-bit
+//             indices in bits 0-23, signs in bits 24-31):
+//             score = n_k/8 (sum T_A + coef sum T_B), coef = alpha g_k (QJL) or
+//             ebar_K. Online softmax in base 2 with a wave-uniform running max
+//             raised only when a tile max exceeds it by more than 2^8.
+//             Values are accumulated one lane per dimension from the
+//             dimension-major V tile; a tile's token weights reach the lanes
+//             through DPP row broadcasts.
 //   merge     waves merge through LDS; splits of a unit merge through a
 //             workspace of (m, l, o) partials written and read with
 //             agent-scope atomics: the last split to finish (atomic counter)
@@ -38,6 +44,7 @@
 // of its decode blocks.
 #include <stdlib.h>
 
+#include "tq_append.hpp"
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
 
@@ -302,58 +309,144 @@ __device__ __forceinline__ void to_float(const RawSlice<N>& r, bool f16, float (
 }
 
 
+// Pointers into the constant address space (4): same 64-bit addresses, but a
+// load through them with a wave-uniform address is always a scalar load.
+#define TQ_CONST __attribute__((address_space(4)))
+typedef const TQ_CONST float cfloat;
+typedef const TQ_CONST int32_t cint32;
+typedef const TQ_CONST int64_t cint64;
+template <class T>
+__device__ __forceinline__ const TQ_CONST T* to_const(const T* p) {
+  return (const TQ_CONST T*)p;
+}
+// Two consecutive floats as one 64-bit scalar load (scalar loads need only
+// 4-byte alignment).
+typedef uint64_t __attribute__((aligned(4))) u64_a4;
+__device__ __forceinline__ uint64_t load_pair(const TQ_CONST float* p) {
+  return *(const TQ_CONST u64_a4*)p;
+}
+__device__ __forceinline__ float2 pair_f2(uint64_t w) {
+  return make_float2(__uint_as_float((uint32_t)w), __uint_as_float((uint32_t)(w >> 32)));
+}
+
+// Eight table levels held in (scalar) registers; pick() selects one per lane
+// by three levels of selects on the index bits, never through memory.
+struct Lut8 {
+  float c0, c1, c2, c3, c4, c5, c6, c7;
+  __device__ __forceinline__ static Lut8 of(const uint64_t (&w)[4]) {
+    const float2 a = pair_f2(w[0]), b = pair_f2(w[1]), c = pair_f2(w[2]), d = pair_f2(w[3]);
+    return Lut8{a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
+  }
+  __device__ __forceinline__ float pick(int i) const {
+    const bool b0 = (i & 1) != 0, b1 = (i & 2) != 0, b2 = (i & 4) != 0;
+    const float p01 = b0 ? c1 : c0, p23 = b0 ? c3 : c2, p45 = b0 ? c5 : c4, p67 = b0 ? c7 : c6;
+    const float p03 = b1 ? p23 : p01, p47 = b1 ? p67 : p45;
+    return b2 ? p47 : p03;
+  }
+};
+
 // ------------------------------------------------------------------ prep kernel
 // Unit of prep block `bid`: the XCD of a unit's decode blocks is
 // (unit * nsplit) / per_xcd; prep blocks are dealt to the same XCD.
+// With APPEND (decode step) the block first stages Pi and S in LDS and,
+// after q^ and u are written, waves 0 and 1 quantize and append the new key
+// and value of the unit with the same functions as the append kernel.
+// F16: q, k, v are fp16 (else fp32). HALF: RoPE pairs (m, m + 32).
+template <bool APPEND, bool F16, bool HALF>
 __global__ __launch_bounds__(256) void decode_prep_kernel(DecodeArgs a, int units, int per_xcd) {
   constexpr int COLS = 16;                 // 4 lanes per row of Pi / S
   __shared__ float s_qh[kDim];
-  const int x = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
-  const int64_t first = ((int64_t)x * per_xcd + a.nsplit - 1) / a.nsplit;
-  const int64_t next = ((int64_t)(x + 1) * per_xcd + a.nsplit - 1) / a.nsplit;
-  const int64_t unit64 = first + j;
-  if (unit64 >= next || unit64 >= units) return;
-  const int unit = (int)unit64;
-  const int h = unit % a.H;
-  const int b = (unit / a.H) % a.B;
-  const int l = a.layer0 + unit / (a.H * a.B);
-  const int lh = l * a.H + h;
-  const int qp = a.q_pos[b];
-  const int n = a.seq_len[b];
-  if (qp < 0 || qp >= a.rope_positions || n <= 0) return;   // the decode kernel writes 0 or NaN
+  __shared__ VectorSmem sm;                // APPEND only (the compiler drops it otherwise)
+  // Every argument field the block reads, in one batch met by one wait (the
+  // asm uses them all), so that no data load waits behind a constant load.
+  const int nsplit = a.nsplit, H = a.H, B = a.B, layer0 = a.layer0, rope_positions = a.rope_positions;
+  const int len_add = a.len_add, max_len = a.max_len;
+  const int64_t slots = a.slots;
+  const uint32_t flags = a.flags;
+  const float *pi_base = a.pi, *s_base = a.qjl_s, *cs_base = a.rope_cs;
+  const void* q_base = a.q;
+  const int32_t *qpos_p = a.q_pos, *len_p = a.seq_len;
+  const int64_t* s0_p = a.seq_slot0;
+  asm volatile("" ::"s"(nsplit), "s"(H), "s"(B), "s"(layer0), "s"(rope_positions), "s"(len_add),
+               "s"(max_len), "s"(slots), "s"(flags), "s"(pi_base), "s"(s_base), "s"(cs_base),
+               "s"(q_base), "s"(qpos_p), "s"(len_p), "s"(s0_p));
+  // (32-bit: the host keeps units * nsplit, and so 8 * per_xcd, below 2^31)
+  const unsigned x = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
+  const unsigned ns = (unsigned)nsplit, px = (unsigned)per_xcd;
+  const unsigned first = (x * px + ns - 1) / ns;
+  const unsigned next = ((x + 1) * px + ns - 1) / ns;
+  const unsigned unit_u = first + j;
+  if (unit_u >= next || unit_u >= (unsigned)units) return;
+  const int unit = (int)unit_u;
+  const int h = unit % H;
+  const int b = (unit / H) % B;
+  const int l = layer0 + unit / (H * B);
+  const int lh = l * H + h;
   const int t = threadIdx.x;
   const int row = t >> 2, c0 = (t & 3) * COLS;
-  const bool paper = (a.flags & kQjlPaper) != 0;
-  const bool half = (a.flags & kRopeHalf) != 0;
-  const bool f16q = a.f16_in != 0;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6), i = t & 63;
+  const bool paper = (flags & kQjlPaper) != 0;
 
-  const float4* pi_row = reinterpret_cast<const float4*>(a.pi + (int64_t)lh * kDim * kDim + row * kDim + c0);
+  // Loads first, none behind a check: Pi and S row slices, q, and for a step
+  // the new key (wave 0) or value (wave 1) with its table levels. Then the
+  // sequence's position, length and first slot (scalar loads, one wait), and
+  // the RoPE row of the position (clamped into the table, so it is requested
+  // as soon as the position arrives, before the checks).
+  const float4* pi_row = reinterpret_cast<const float4*>(pi_base + (int64_t)lh * kDim * kDim + row * kDim + c0);
+  const float4* s_row = reinterpret_cast<const float4*>(s_base + row * kDim + c0);
   float4 pr[COLS / 4], sr[COLS / 4];
 #pragma unroll
   for (int k = 0; k < COLS / 4; ++k) pr[k] = pi_row[k];
-  if (!paper) {
-    const float4* s_row = reinterpret_cast<const float4*>(a.qjl_s + row * kDim + c0);
 #pragma unroll
-    for (int k = 0; k < COLS / 4; ++k) sr[k] = s_row[k];
-  }
-  const float4* cs_row = reinterpret_cast<const float4*>(a.rope_cs + (int64_t)qp * 2 * kPairs);
+  for (int k = 0; k < COLS / 4; ++k) sr[k] = s_row[k];
   RawSlice<COLS> qraw, praw;
-  load_raw<COLS>(a.q, (int64_t)unit * kDim + c0, f16q, qraw);
-  if (half) load_raw<COLS>(a.q, (int64_t)unit * kDim + (c0 ^ 32), f16q, praw);
+  load_raw<COLS>(q_base, (int64_t)unit * kDim + c0, F16, qraw);
+  if (HALF) load_raw<COLS>(q_base, (int64_t)unit * kDim + (c0 ^ 32), F16, praw);
+  float xa = 0.0f;
+  Levels La{};
+  if (APPEND) {
+    xa = load_in(wave == 1 ? a.v_new : a.k_new, (int64_t)unit * kDim + i, F16);
+    La = load_levels((wave == 1 ? a.lut_v : a.lut_k) + lh * 8);
+  }
+  const int qp = to_const(qpos_p)[b];
+  const int len = to_const(len_p)[b];
+  const int64_t s0 = to_const(s0_p)[b];
+  asm volatile("" ::"s"(qp), "s"(len), "s"(s0));
+  const int qpc = min(max(qp, 0), rope_positions - 1);
+  const float4* cs_row = reinterpret_cast<const float4*>(cs_base + (int64_t)qpc * 2 * kPairs);
   float4 csv[COLS / 2];
-  if (half) {
+  if (HALF) {
 #pragma unroll
     for (int k = 0; k < COLS / 2; ++k) csv[k] = cs_row[(c0 & 31) / 2 + k];   // pairs (c0 & 31) ..
   } else {
 #pragma unroll
     for (int k = 0; k < COLS / 4; ++k) csv[k] = cs_row[c0 / 4 + k];          // pairs c0/2 ..
   }
+  float2 csk = make_float2(1.0f, 0.0f);
+  if (APPEND)
+    csk = reinterpret_cast<const float2*>(cs_base + (int64_t)qpc * 2 * kPairs)[HALF ? (i & 31) : (i >> 1)];
+
+  const int n = len + len_add;             // tokens attended
+  if (qp < 0 || qp >= rope_positions || n <= 0) return;   // the decode kernel writes 0 or NaN
+  // the new token goes to slot s0 + len exactly when the decode kernel will
+  // accept the sequence (it checks the same bounds for n = len + 1)
+  const bool do_append = APPEND && len >= 0 && n <= max_len && s0 >= 0 && (s0 & 63) == 0 &&
+                         s0 + n <= slots;
+  if (do_append) {
+    // Pi and S for the wave-per-vector quantizer: this thread holds columns
+    // c0 .. c0 + 15 of row `row`
+#pragma unroll
+    for (int k = 0; k < COLS / 4; ++k) {
+      stage_row4(sm.pi, row, c0 + 4 * k, pr[k]);
+      stage_row4(sm.s, row, c0 + 4 * k, sr[k]);
+    }
+  }
 
   // q' = RoPE(q) in registers (x'_a = x_a c - x_b s, x'_b = x_a s + x_b c)
   float qx[COLS], qy[COLS], qr[COLS];
-  to_float<COLS>(qraw, f16q, qx);
-  if (half) {
-    to_float<COLS>(praw, f16q, qy);
+  to_float<COLS>(qraw, F16, qx);
+  if (HALF) {
+    to_float<COLS>(praw, F16, qy);
 #pragma unroll
     for (int k = 0; k < COLS; ++k) {
       const float4 v = csv[k / 2];
@@ -399,8 +492,20 @@ __global__ __launch_bounds__(256) void decode_prep_kernel(DecodeArgs a, int unit
     u_row = up;
   }
   if ((t & 3) == 1) qu[kDim + row] = u_row;
-}
 
+  if (do_append) {
+    lds_barrier();                     // Pi and S staged
+    if (wave < 2) {
+      const bool is_v = wave == 1;
+      const int ksign = paper ? 2 : 1;
+      const int sign_mode = is_v ? ((a.flags & kVQjl) ? ksign : 0) : ksign;
+      const bool rotate = !is_v || (a.flags & kVRotate);
+      const float xr = is_v ? xa : rope_wave(xa, csk, HALF, i);
+      append_wave(xr, is_v, rotate, La, sm, sign_mode, s0 + len, lh, const_cast<uint8_t*>(a.k_codes),
+                  const_cast<uint8_t*>(a.v_codes), const_cast<uint16_t*>(a.scalars), a.slots, i, wave);
+    }
+  }
+}
 
 
 template <int WAVES, bool VQJL>
@@ -426,21 +531,102 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   const int bid = blockIdx.x;
   const int work = (bid % kXcds) * per_xcd + bid / kXcds;
   if (work >= total_work) return;
-  const int unit = work / a.nsplit;
-  const int split = work - unit * a.nsplit;
-  const int h = unit % a.H;
-  const int b = (unit / a.H) % a.B;
-  const int li = unit / (a.H * a.B);
-  const int l = a.layer0 + li;
-  const int lh = l * a.H + h;
+  // The argument fields the prologue needs, read in one batch and met by one
+  // wait (used by the asm), so that no later data load waits on one of them.
+  const int nsplit = a.nsplit, H = a.H, B = a.B, layer0 = a.layer0;
+  const uint32_t flags = a.flags;
+  const float *qu_base = a.qu, *lut_k = a.lut_k, *lut_v = a.lut_v, *ebar = a.ebar;
+  const int32_t* seq_len = a.seq_len;
+  const int64_t* seq_slot0 = a.seq_slot0;
+  const int32_t* q_pos = a.q_pos;
+  asm volatile("" ::"s"(nsplit), "s"(H), "s"(B), "s"(layer0), "s"(flags), "s"(qu_base), "s"(lut_k),
+               "s"(lut_v), "s"(ebar), "s"(seq_len), "s"(seq_slot0), "s"(q_pos));
+  const int unit = work / nsplit;
+  const int split = work - unit * nsplit;
+  const int h = unit % H;
+  const int b = (unit / H) % B;
+  const int li = unit / (H * B);
+  const int l = layer0 + li;
+  const int lh = l * H + h;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
 
-  const int n = a.seq_len[b];
-  const int64_t s0 = a.seq_slot0[b];
-  const int qp = a.q_pos[b];
-  const bool valid = n >= 0 && n <= a.max_len && s0 >= 0 && (s0 & 63) == 0 &&
-                     s0 + n <= a.slots && qp >= 0 && qp < a.rope_positions;
+  const bool paper = (flags & kQjlPaper) != 0;
+
+  // ------------------------------------------------------- prologue loads
+  // Everything the prologue reads is the same for a whole wave and is fetched
+  // with scalar loads, issued before anything else and before the first store
+  // of the kernel (so the compiler may take the scalar path): the scalar cache
+  // does not queue behind the tile loads that blocks already running on this
+  // compute unit have in its vector memory pipeline, which can hold a late
+  // block's first vector load for several microseconds.
+  // Table entries built by this thread (NT threads):
+  //   ta (2048 entries): e = t + NT m, pair P = e / 64 = wave + NT/64 m, index f = e % 64 = lane
+  //   tb (2048 entries in groups of 4): group e = t + NT m of word w = e / 64,
+  //      sign bytes 4 (e % 64) .. 4 (e % 64) + 3
+  // Read through the constant address space: loads from it with a wave-uniform
+  // address always take the scalar path. (Nothing here changes during a launch:
+  // q^ and u come from the preceding prep kernel.)
+  const cfloat* p_qu = to_const(qu_base);
+  const cfloat* p_lk = to_const(lut_k);
+  const cfloat* p_lv = to_const(lut_v);
+  const cfloat* p_eb = to_const(ebar);
+  const cint32* p_len = to_const(seq_len);
+  const cint64* p_s0 = to_const(seq_slot0);
+  const cint32* p_qp = to_const(q_pos);
+  const cfloat* qu = p_qu + (int64_t)unit * 2 * kDim;
+  const cfloat* lk = p_lk + lh * 8;
+  const cfloat* lv = p_lv + lh * 8;
+  // Loaded as 64-bit pairs: one asm operand each (an asm takes at most 30).
+  uint64_t qw[TAM], uw[TBM][4], kw[4], vw[4];
+#pragma unroll
+  for (int m = 0; m < TAM; ++m) qw[m] = load_pair(qu + 2 * (wave + (NT / 64) * m));
+#pragma unroll
+  for (int m = 0; m < TBM; ++m) {
+    const cfloat* e = qu + kDim + 8 * (wave + (NT / 64) * m);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) uw[m][k] = load_pair(e + 2 * k);
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    kw[k] = load_pair(lk + 2 * k);
+    vw[k] = load_pair(lv + 2 * k);
+  }
+  const float ebar_raw = *(paper ? p_eb + lh * 2 : lk);
+  const int n = p_len[b] + a.len_add;
+  const int64_t s0 = p_s0[b];
+  const int qp = p_qp[b];
+  // Every loaded value is used here, before the checks branch: the loads are
+  // independent, so they are all issued and met by one wait (a load is
+  // otherwise free to sink below the branch, one round trip after the other).
+  static_assert(TAM + 4 * TBM + 8 + 4 <= 30, "asm operand limit");
+  if constexpr (TBM == 1) {
+    asm volatile("" ::"s"(qw[0]), "s"(qw[1]), "s"(qw[2]), "s"(qw[3]), "s"(uw[0][0]), "s"(uw[0][1]),
+                 "s"(uw[0][2]), "s"(uw[0][3]), "s"(kw[0]), "s"(kw[1]), "s"(kw[2]), "s"(kw[3]),
+                 "s"(vw[0]), "s"(vw[1]), "s"(vw[2]), "s"(vw[3]), "s"(ebar_raw), "s"(n), "s"(s0),
+                 "s"(qp));
+  } else {
+    asm volatile("" ::"s"(qw[0]), "s"(qw[1]), "s"(qw[2]), "s"(qw[3]), "s"(qw[4]), "s"(qw[5]),
+                 "s"(qw[6]), "s"(qw[7]), "s"(uw[0][0]), "s"(uw[0][1]), "s"(uw[0][2]),
+                 "s"(uw[0][3]), "s"(uw[1][0]), "s"(uw[1][1]), "s"(uw[1][2]), "s"(uw[1][3]),
+                 "s"(kw[0]), "s"(kw[1]), "s"(kw[2]), "s"(kw[3]), "s"(vw[0]), "s"(vw[1]),
+                 "s"(vw[2]), "s"(vw[3]), "s"(ebar_raw), "s"(n), "s"(s0), "s"(qp));
+  }
+  float2 qpair[TAM];
+#pragma unroll
+  for (int m = 0; m < TAM; ++m) qpair[m] = pair_f2(qw[m]);
+  float4 ulo[TBM], uhi[TBM];
+#pragma unroll
+  for (int m = 0; m < TBM; ++m) {
+    const float2 a0 = pair_f2(uw[m][0]), a1 = pair_f2(uw[m][1]);
+    const float2 a2 = pair_f2(uw[m][2]), a3 = pair_f2(uw[m][3]);
+    ulo[m] = make_float4(a0.x, a0.y, a1.x, a1.y);
+    uhi[m] = make_float4(a2.x, a2.y, a3.x, a3.y);
+  }
+  const Lut8 ck = Lut8::of(kw), cvl = Lut8::of(vw);
+  const float ebar_k = paper ? ebar_raw : 0.0f;
+  const bool valid = (n >= 0) & (n <= a.max_len) & (s0 >= 0) & ((s0 & 63) == 0) &
+                     (s0 + n <= a.slots) & (qp >= 0) & (qp < a.rope_positions);
   if (!valid || n == 0) {
     if (split == 0 && t < kDim) store_out(a, unit, t, valid ? 0.0f : __int_as_float(0x7FC00000));
     return;
@@ -450,43 +636,13 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   if (tile_begin >= ntiles) return;
   const int tile_end = min(ntiles, tile_begin + a.split_tiles);
   const int participants = (ntiles + a.split_tiles - 1) / a.split_tiles;
-  const bool paper = (a.flags & kQjlPaper) != 0;
-
-  // ------------------------------------------- loads, in the order they are needed
-  // Table entries built by this thread (NT threads):
-  //   ta (2048 entries): e = t + NT m, pair P = e / 64, index f = e % 64 = t % 64
-  //   tb (2048 entries in groups of 4): group e = t + NT m of word w = e / 64,
-  //      sign bytes 4 (e % 64) .. 4 (e % 64) + 3
-  const float* qu = a.qu + (int64_t)unit * 2 * kDim;
-  const int f_ta = t & 63;
-  const float ck_lo = a.lut_k[lh * 8 + (f_ta & 7)];
-  const float ck_hi = a.lut_k[lh * 8 + (f_ta >> 3)];
-  float2 qpair[TAM];
-#pragma unroll
-  for (int m = 0; m < TAM; ++m) qpair[m] = reinterpret_cast<const float2*>(qu)[(t >> 6) + (NT / 64) * m];
-  float4 ulo[TBM], uhi[TBM];
-#pragma unroll
-  for (int m = 0; m < TBM; ++m) {
-    const int w = (t + NT * m) >> 6;
-    ulo[m] = reinterpret_cast<const float4*>(qu + kDim)[2 * w];
-    uhi[m] = reinterpret_cast<const float4*>(qu + kDim)[2 * w + 1];
-  }
-  const float cv = a.lut_v[lh * 8 + (t & 7)];
-  // (every prologue load is unconditional: a load under a branch makes the
-  // compiler's wait counts after the join conservative)
-  const float ebar_raw = *(paper ? a.ebar + lh * 2 : a.lut_k + lh * 8);
-  const float ebar_k = paper ? ebar_raw : 0.0f;
+  const float ck_lo = ck.pick(lane & 7), ck_hi = ck.pick(lane >> 3);
+  const float cv = cvl.pick(t & 7);
 
   const uint8_t* kreg = a.k_codes + (int64_t)lh * a.slots * 32;
   const uint8_t* vreg = a.v_codes + (int64_t)lh * a.slots * 32;
   const uint2* sreg = reinterpret_cast<const uint2*>(a.scalars + (int64_t)lh * a.slots * 4);
   const int64_t tile0 = s0 >> 6;
-  TileRegs buf[DEPTH];
-#pragma unroll
-  for (int d = 0; d < DEPTH; ++d) {
-    const int tq = min(tile_begin + wave + d * WAVES, tile_end - 1);   // (a wave without tiles re-reads one)
-    load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
-  }
   // --------------------------------------------------------------- prologue
 #pragma unroll
   for (int m = 0; m < TAM; ++m)
@@ -506,6 +662,15 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     reinterpret_cast<float4*>(s_tb)[e] = v;
   }
   s_vtab[t & 15] = cv;             // every thread: identical values, no branch around the load
+  // The first tiles are requested only now: issuing a vector load can stall
+  // while this compute unit's memory pipeline is full, and the tables above
+  // need nothing from it.
+  TileRegs buf[DEPTH];
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) {
+    const int tq = min(tile_begin + wave + d * WAVES, tile_end - 1);   // (a wave without tiles re-reads one)
+    load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
+  }
   lds_barrier();
 
   // Pi for the epilogue, straight into LDS (1 KB per wave instruction). Issued
@@ -742,8 +907,19 @@ hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st) {
   const bool vq = (a.flags & kVQjl) != 0;
   // prep blocks: per XCD, the units whose decode blocks run there
   const int64_t prep_per_xcd = (per_xcd + a.nsplit - 1) / a.nsplit + 1;
-  hipLaunchKernelGGL(decode_prep_kernel, dim3((unsigned)(kXcds * prep_per_xcd)), dim3(256), 0, st, a,
-                     (int)units, (int)per_xcd);
+  {
+    const dim3 pg((unsigned)(kXcds * prep_per_xcd)), pb(256);
+    const bool f16 = a.f16_in != 0, half = (a.flags & kRopeHalf) != 0;
+#define TQ_PREP(AP, F, HF) hipLaunchKernelGGL((decode_prep_kernel<AP, F, HF>), pg, pb, 0, st, a, (int)units, (int)per_xcd)
+    if (a.append) {
+      if (f16) { if (half) TQ_PREP(true, true, true); else TQ_PREP(true, true, false); }
+      else     { if (half) TQ_PREP(true, false, true); else TQ_PREP(true, false, false); }
+    } else {
+      if (f16) { if (half) TQ_PREP(false, true, true); else TQ_PREP(false, true, false); }
+      else     { if (half) TQ_PREP(false, false, true); else TQ_PREP(false, false, false); }
+    }
+#undef TQ_PREP
+  }
   if (waves == 8) {
     if (vq)
       hipLaunchKernelGGL((decode_kernel<8, true>), dim3((unsigned)blocks), dim3(512), 0, st, a, (int)total, (int)per_xcd);

@@ -56,6 +56,13 @@ struct DecodeArgs {
   uint32_t* counters;      // [units]
   int nsplit;              // splits per unit
   int split_tiles;         // 64-token tiles per split
+  // decode step: the prep kernel first appends one token per sequence (its key
+  // and value [nlayers][B][H][64], position q_pos[b], slot seq_slot0[b] +
+  // seq_len[b]); the attention then covers seq_len[b] + len_add tokens
+  const void* k_new;
+  const void* v_new;
+  int append;
+  int len_add;
 };
 
 constexpr int kPartialFloats = 2 * 64 + 4;   // m, l, pad, pad, o[64], s[64]

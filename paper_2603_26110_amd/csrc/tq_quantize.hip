@@ -12,6 +12,7 @@
 // Both evaluate the rotation as an fma chain over k ascending and the
 // quantizer steps with the fixed binary32 order of quantize_lane, so a token
 // gets the same codes from either kernel.
+#include "tq_append.hpp"
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
 
@@ -85,18 +86,6 @@ __device__ __forceinline__ void rotate_lane(float (&x)[kDim], const float* s_pi,
   }
 #pragma unroll
   for (int i = 0; i < kDim; ++i) x[i] = s_col[i * kDim + lane];
-}
-
-// Write one dimension-major V nibble group: `mask` selects the nibbles of
-// `word` this writer owns. Whole words are stored; partial words are merged
-// with atomics so concurrent writers of neighbouring slots do not collide.
-__device__ __forceinline__ void store_v_word(uint32_t* addr, uint32_t word, uint32_t mask) {
-  if (mask == 0xFFFFFFFFu) {
-    *addr = word;
-  } else if (mask != 0u) {
-    atomicAnd(addr, ~mask);
-    atomicOr(addr, word & mask);
-  }
 }
 
 // ----------------------------------------------------- lane-per-token kernel
@@ -203,91 +192,9 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
 }
 
 // ----------------------------------------------- wave-per-vector kernel
-// Block: 2 waves for one (layer, sequence, token, head): wave 0 quantizes the
-// key, wave 1 the value; lane = dimension. Pi and S are read with coalesced
-// 16-byte loads by the whole block and stored transposed in LDS (rows padded
-// to 65 floats), so that lane i walks column i of the transpose, i.e. row i of
-// the matrix, with conflict-free reads; the fma chains keep k ascending.
-constexpr int kTStride = kDim + 1;
-
-struct VectorSmem {
-  float piT[kDim * kTStride];   // piT[k * 65 + i] = Pi[i][k]
-  float sT[kDim * kTStride];    // sT[k * 65 + i] = S[i][k]
-  float x[2][kDim];
-  float r[2][kDim];
-};
-
-__device__ __forceinline__ void wave_sync_lds() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// Row i of a 64 x 64 matrix (stored transposed in `mT`) times the vector
-// staged in `v`: fma chain over k ascending, the order of rotate_lane and
-// quantize_lane.
-__device__ __forceinline__ float row_dot_t(const float* mT, const float* v, int i) {
-  float acc = 0.0f;
-#pragma unroll
-  for (int k4 = 0; k4 < kDim / 4; ++k4) {
-    const float4 vv = reinterpret_cast<const float4*>(v)[k4];
-    acc = fmaf(mT[(4 * k4 + 0) * kTStride + i], vv.x, acc);
-    acc = fmaf(mT[(4 * k4 + 1) * kTStride + i], vv.y, acc);
-    acc = fmaf(mT[(4 * k4 + 2) * kTStride + i], vv.z, acc);
-    acc = fmaf(mT[(4 * k4 + 3) * kTStride + i], vv.w, acc);
-  }
-  return acc;
-}
-
-// Quantize the vector whose element i lane i holds in `xh`; same arithmetic
-// order as quantize_lane. Returns the lane's nibble; n16/g16 are uniform.
-__device__ __forceinline__ uint32_t quantize_wave(float xh, const Levels& L,
-                                                  const float* sT, int sign_mode, float* xs,
-                                                  float* rs, int i, uint32_t* n16, uint32_t* g16) {
-  xs[i] = xh;
-  wave_sync_lds();
-  float s = 0.0f;
-#pragma unroll
-  for (int k4 = 0; k4 < kDim / 4; ++k4) {
-    const float4 v = reinterpret_cast<const float4*>(xs)[k4];
-    s = fmaf(v.x, v.x, s);
-    s = fmaf(v.y, v.y, s);
-    s = fmaf(v.z, v.z, s);
-    s = fmaf(v.w, v.w, s);
-  }
-  const float n = sqrtf(s);
-  const float inv = (n == 0.0f) ? 0.0f : 8.0f / n;
-  const float u = xh * inv;
-  TQ_PIN_LEVELS(L);
-  uint32_t idx;
-  const float lv = nearest_level(u, TQ_LEVELS(L), &idx);
-  const float r = u - lv;
-  rs[i] = r;
-  wave_sync_lds();
-  float gs = 0.0f;
-#pragma unroll
-  for (int k4 = 0; k4 < kDim / 4; ++k4) {
-    const float4 v = reinterpret_cast<const float4*>(rs)[k4];
-    gs = fmaf(v.x, v.x, gs);
-    gs = fmaf(v.y, v.y, gs);
-    gs = fmaf(v.z, v.z, gs);
-    gs = fmaf(v.w, v.w, gs);
-  }
-  const float g = sqrtf(gs);
-  uint32_t bit = 0;
-  if (sign_mode == 1) {
-    bit = (row_dot_t(sT, rs, i) < 0.0f) ? 0u : 1u;
-  } else if (sign_mode == 2) {
-    bit = (r < 0.0f) ? 0u : 1u;
-  }
-  *n16 = store_norm(n);
-  *g16 = (sign_mode == 0) ? 0u : store_norm(g);
-  return idx | (bit << 3);
-}
-
-// Coalesced copy of a 64 x 64 row-major matrix into its padded transpose, in
-// two steps so that the loads can be issued early: thread t holds float4
-// number t + 128 j (row e / 16, columns 4 (e % 16) .. 4 (e % 16) + 3).
+// Coalesced copy of a 64 x 64 row-major matrix into its staged form, in two
+// steps so that the loads can be issued early: thread t holds float4 number
+// t + 128 j (row e / 16, columns 4 (e % 16) .. 4 (e % 16) + 3).
 struct MatrixSlice {
   float4 v[8];
 };
@@ -297,14 +204,11 @@ __device__ __forceinline__ void load_slice(const float* __restrict__ m, MatrixSl
   for (int j = 0; j < 8; ++j) sl.v[j] = reinterpret_cast<const float4*>(m)[t + 128 * j];
 }
 
-__device__ __forceinline__ void store_slice_transposed(const MatrixSlice& sl, float* mT, int t) {
+__device__ __forceinline__ void store_slice(const MatrixSlice& sl, float* m, int t) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const int e = t + 128 * j, row = e >> 4, col = (e & 15) * 4;
-    mT[(col + 0) * kTStride + row] = sl.v[j].x;
-    mT[(col + 1) * kTStride + row] = sl.v[j].y;
-    mT[(col + 2) * kTStride + row] = sl.v[j].z;
-    mT[(col + 3) * kTStride + row] = sl.v[j].w;
+    const int e = t + 128 * j;
+    stage_row4(m, e >> 4, (e & 15) * 4, sl.v[j]);
   }
 }
 
@@ -349,52 +253,14 @@ __global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, uint
     const int m = half ? (i & 31) : (i >> 1);
     cs = reinterpret_cast<const float2*>(a.rope_cs + (int64_t)pos * 2 * kPairs)[m];
   }
-  if (any_rotate) store_slice_transposed(pi_sl, sm.piT, threadIdx.x);
-  if (any_proj) store_slice_transposed(s_sl, sm.sT, threadIdx.x);
+  if (any_rotate) store_slice(pi_sl, sm.pi, threadIdx.x);
+  if (any_proj) store_slice(s_sl, sm.s, threadIdx.x);
   __syncthreads();
 
-  // ---- RoPE (keys) and rotation
-  if (!is_v && !rotated) {
-    const int partner = half ? (i ^ 32) : (i ^ 1);
-    const bool first = half ? (i < 32) : ((i & 1) == 0);
-    const float xp = __shfl(x, partner, 64);
-    // pair (a, b): x'_a = x_a c - x_b s, x'_b = x_a s + x_b c
-    x = first ? (x * cs.x - xp * cs.y) : (xp * cs.y + x * cs.x);
-  }
-  float* xs = sm.x[wave];
-  float* rs = sm.r[wave];
-  if (rotate) {
-    xs[i] = x;
-    wave_sync_lds();
-    x = row_dot_t(sm.piT, xs, i);
-    wave_sync_lds();   // xs is rewritten by quantize_wave
-  }
-
-  uint32_t n16, g16;
-  const uint32_t nib = quantize_wave(x, L, sm.sT, sign_mode, xs, rs, i, &n16, &g16);
-  const int64_t tile = slot >> 6;
-  const int r = (int)(slot & 63);
-  if (!is_v) {
-    // key: token-major key words (index bits 3j, sign bit 24 + j); lane 8w
-    // ends with word w
-    uint32_t word = key_code_bits(nib & 7u, nib >> 3, i & 7);
-    word |= __shfl_xor(word, 1, 64);
-    word |= __shfl_xor(word, 2, 64);
-    word |= __shfl_xor(word, 4, 64);
-    uint8_t* kreg = a.k_codes + lh * a.slots * 32;
-    if ((i & 7) == 0) {
-      const int w = i >> 3;
-      *reinterpret_cast<uint32_t*>(kreg + tile_half_offset(tile, w >> 2, r) + (w & 3) * 4) = word;
-    }
-    if (i == 0) reinterpret_cast<uint32_t*>(a.scalars + (lh * a.slots + slot) * 4)[0] = n16 | (g16 << 16);
-  } else {
-    // value: dimension-major, one nibble of dimension i's word for this slot
-    uint8_t* vreg = a.v_codes + lh * a.slots * 32;
-    const int cc = r >> 5, G4 = (r & 31) >> 3, jj = r & 7;
-    uint32_t* addr = reinterpret_cast<uint32_t*>(vreg + tile_half_offset(tile, cc, i) + G4 * 4);
-    store_v_word(addr, nib << (4 * jj), 15u << (4 * jj));
-    if (i == 0) reinterpret_cast<uint32_t*>(a.scalars + (lh * a.slots + slot) * 4)[1] = n16 | (g16 << 16);
-  }
+  // ---- RoPE (keys), rotation, quantizer, store
+  if (!is_v && !rotated) x = rope_wave(x, cs, half, i);
+  append_wave(x, is_v, rotate, L, sm, sign_mode, slot, lh, a.k_codes, a.v_codes, a.scalars, a.slots, i,
+              wave);
 }
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t st) {

@@ -37,7 +37,7 @@ def _defines():
 
 def test_header_declares_the_entry_points():
     assert _declared_functions() == sorted([
-        "tq_cache_bytes", "tq_rope_table", "tq_quantize_pack", "tq_decode_attend",
+        "tq_cache_bytes", "tq_rope_table", "tq_quantize_pack", "tq_decode_attend", "tq_decode_step",
         "tq_decode_workspace_bytes", "tq_calibrate_rotation", "tq_last_error", "tq_version"])
 
 
@@ -193,3 +193,21 @@ def test_rope_table_and_calibration_argument_checks():
     assert L.tq_calibrate_rotation(None, 2, 10, None, None, None) == -1
     assert L.tq_calibrate_rotation(P(FAKE), 2, 0, P(FAKE), None, None) == -1
     assert L.tq_calibrate_rotation(P(FAKE), -1, 10, P(FAKE), None, None) == -1
+
+
+def _step(p, c, B=1, max_len=64, kv=FAKE, ws=None, ws_bytes=0, ptrs=FAKE, out=FAKE):
+    L = tq._load()
+    P = ctypes.c_void_p
+    return L.tq_decode_step(ctypes.byref(p), ctypes.byref(c), P(ptrs), P(kv), P(kv), B, 0, 1, P(ptrs),
+                            P(ptrs), P(ptrs), max_len, P(ptrs), P(ptrs), P(ptrs), P(ptrs), None, P(out),
+                            P(ws) if ws else None, ws_bytes, None)
+
+
+def test_decode_step_argument_checks():
+    assert _step(_params(flags=1 | 16), _cache()) == -1
+    assert "TQ_INPUT_ROTATED" in tq.last_error()
+    assert _step(_params(), _cache(), max_len=0) == -1 and "max_len" in tq.last_error()
+    assert _step(_params(), _cache(), kv=0) == -1 and "k and v" in tq.last_error()
+    assert _step(_params(), _cache(), kv=FAKE + 4) == -3
+    assert _step(_params(), _cache(), max_len=129) == -5
+    assert _step(_params(), _cache(), B=0) == 0
