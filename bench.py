@@ -223,6 +223,7 @@ def main():
         alg_bytes = kv_bytes + pi_bytes + 64 * 64 * 4 + units * 8 * 4 * 2 + units * 64 * io_b * 2
     achieved = alg_bytes / (step_ms * 1e-3) / 1e9
     value = kv_bytes / (ms_per_step * 1e-3) / 1e9
+    traffic, traffic_src = (None, None) if args.decode_only else measured_traffic(wl.name)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -250,7 +251,8 @@ def main():
         "two_call_step_ms": None if two_call_ms is None else round(two_call_ms, 5),
         "decode_attend_ms": round(attend_ms, 5),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "traffic_source": traffic_src,
                      "kernel": ("decode_attend: prep + attention kernels" if args.decode_only else
                                 "decode_step: step prologue + attention kernels"),
                      "alg_bytes_per_launch": int(alg_bytes)},
@@ -260,6 +262,25 @@ def main():
                                               "NVIDIA GPU on Colab, model and precision unstated (Table 6)"},
     }
     print(json.dumps(line))
+
+
+def measured_traffic(workload):
+    """HBM bytes per step of the decode-step kernels from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy's readings), or
+    None when the kernel sources have changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", f"decode_step_traffic__{workload}.json")
+    if not os.path.exists(path):
+        return None, None
+    with open(path) as f:
+        rec = json.load(f)
+    h = hashlib.sha256()
+    for src in rec["sources"]:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != rec["sources_sha256"]:
+        return None, None
+    return int(rec["traffic_bytes_per_step"]), os.path.relpath(path, ROOT)
 
 
 def cpu_baseline(tq, params, rep, S, lut, pi, q, L, H, slots, n_ctx, seconds):
