@@ -151,3 +151,48 @@ def as_io(x: np.ndarray, io_dtype: str) -> np.ndarray:
     if io_dtype == "f16":
         return x.astype(np.float16)
     return x.astype(np.float32)
+
+
+# ---------------------------------------------------------------------------
+# The same distributions drawn on a torch device, for workloads too large to
+# draw on the host (the ESM-2 3B shape has 2.7e9 key and value elements).
+# Seeded by (seed, layer) so that one layer can be drawn at a time; the
+# streams differ from the NumPy ones above, the distributions do not.
+# ---------------------------------------------------------------------------
+def device_generator(seed: int, layer: int, device):
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1000003 + int(layer))
+    return g
+
+
+def keys_on(gen, batch: int, tokens: int, heads: int, channels_lh: np.ndarray, dtype, device):
+    """[batch][tokens][heads][64] keys of one layer: N(0, 1), the 4 outlier
+    channels of each head (channels_lh [heads][4]) scaled x20."""
+    import torch
+    k = torch.randn((batch, tokens, heads, HEAD_DIM), generator=gen, device=device, dtype=torch.float32)
+    scale = torch.ones((heads, HEAD_DIM), dtype=torch.float32)
+    for h in range(heads):
+        scale[h, torch.as_tensor(channels_lh[h])] = OUTLIER_SCALE
+    k *= scale.to(device)
+    return k.to(dtype)
+
+
+def values_on(gen, batch: int, tokens: int, heads: int, dtype, device):
+    """[batch][tokens][heads][64] Student-t (4 degrees of freedom) values of
+    one layer: z0 / sqrt((z1^2 + z2^2 + z3^2 + z4^2) / 4) with z ~ N(0, 1)."""
+    import torch
+    shape = (batch, tokens, heads, HEAD_DIM)
+    chi = torch.zeros(shape, device=device, dtype=torch.float32)
+    for _ in range(int(STUDENT_T_DOF)):
+        z = torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+        chi.addcmul_(z, z)
+    z0 = torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+    return (z0 / torch.sqrt(chi / STUDENT_T_DOF)).to(dtype)
+
+
+def queries_on(gen, batch: int, heads: int, dtype, device):
+    """[batch][heads][64] N(0, 1) queries of one layer."""
+    import torch
+    return torch.randn((batch, heads, HEAD_DIM), generator=gen, device=device,
+                       dtype=torch.float32).to(dtype)
