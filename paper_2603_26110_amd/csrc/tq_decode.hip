@@ -805,18 +805,46 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     lds_barrier();
     if (!s_last) return;
     if (t < kDim) {
-      float* base = a.partials + (int64_t)unit * a.nsplit * kPartialFloats;
-      M = -INFINITY;
-      for (int s = 0; s < participants; ++s)
-        M = fmaxf(M, __hip_atomic_load(base + s * kPartialFloats, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-      L = 0.0f; O = 0.0f; SG = 0.0f;
-      for (int s = 0; s < participants; ++s) {
-        float* ps = base + s * kPartialFloats;
-        const float f = __builtin_amdgcn_exp2f(__hip_atomic_load(ps, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) - M);
-        L += __hip_atomic_load(ps + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
-        O += __hip_atomic_load(ps + 4 + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
-        if (VQJL) SG += __hip_atomic_load(ps + 4 + kDim + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) * f;
+      // Wave 0 merges. Lane p holds split p's (m, l) (64 splits at a time);
+      // the o rows are fetched 8 splits per batch with the batch's loads in
+      // flight together (a loop that used each load before issuing the next
+      // would pay one memory round trip per split).
+      const float* base = a.partials + (int64_t)unit * a.nsplit * kPartialFloats;
+      float Mw = -INFINITY;
+      for (int p0 = 0; p0 < participants; p0 += 64) {
+        const int pc = min(p0 + lane, participants - 1);
+        Mw = fmaxf(Mw, __hip_atomic_load(base + (int64_t)pc * kPartialFloats, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT));
       }
+      M = wave_max_uniform(Mw);
+      float Ll = 0.0f;
+      O = 0.0f; SG = 0.0f;
+      for (int p0 = 0; p0 < participants; p0 += 64) {
+        const int cnt = min(64, participants - p0);
+        const float* pp = base + (int64_t)min(p0 + lane, participants - 1) * kPartialFloats;
+        const float mp = __hip_atomic_load(pp, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const float lp = __hip_atomic_load(pp + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const float f = (lane < cnt && mp != -INFINITY) ? __builtin_amdgcn_exp2f(mp - M) : 0.0f;
+        Ll = fmaf(f, lp, Ll);
+        const int fi = __float_as_int(f);
+        for (int q0 = 0; q0 < cnt; q0 += 8) {
+          float ov[8], sv[8];
+#pragma unroll
+          for (int r = 0; r < 8; ++r) {
+            const float* pq = base + (int64_t)(p0 + min(q0 + r, cnt - 1)) * kPartialFloats;
+            ov[r] = __hip_atomic_load(pq + 4 + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (VQJL) sv[r] = __hip_atomic_load(pq + 4 + kDim + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+#pragma unroll
+          for (int r = 0; r < 8; ++r) {
+            // weight of split p0 + q0 + r (0 past the last: lanes >= cnt hold f = 0)
+            const float fq = __int_as_float(__builtin_amdgcn_readlane(fi, min(q0 + r, 63)));
+            O = fmaf(fq, ov[r], O);
+            if (VQJL) SG = fmaf(fq, sv[r], SG);
+          }
+        }
+      }
+      L = wave_sum_uniform(Ll);
     }
     // leave the workspace zeroed for the next call
     if (t == 0) __hip_atomic_store(a.counters + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
