@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--replicas", type=int, default=0,
                     help="number of input replicas (default: enough for --replica-bytes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fp16-baseline", action="store_true",
+                    help="skip the plain fp16 attention timing (PyTorch) printed for context")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-probe", type=int, default=0,
                     help="only run a plain device copy of this many MiB (counter calibration)")
@@ -225,6 +227,12 @@ def main():
     value = kv_bytes / (ms_per_step * 1e-3) / 1e9
     traffic, traffic_src = (None, None) if args.decode_only else measured_traffic(wl.name)
 
+    fp16_base = None if args.decode_only or args.no_fp16_baseline else fp16_attention_baseline(
+        torch, L * H, n_ctx, args.replica_bytes, K)
+    if fp16_base:
+        fp16_base["decode_attend_speedup_vs_sdpa"] = round(fp16_base["sdpa_ms"] / attend_ms, 2)
+        fp16_base["decode_step_speedup_vs_sdpa"] = round(fp16_base["sdpa_ms"] / step_ms, 2)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(tq, params, reps[0], S, lut, pi, q, L, H, slots, n_ctx, args.cpu_seconds)
@@ -257,11 +265,56 @@ def main():
                                 "decode_step: step prologue + attention kernels"),
                      "alg_bytes_per_launch": int(alg_bytes)},
         "cpu_baseline": cpu,
+        "fp16_attention_baseline": fp16_base,
         "paper_context": {"memory_reduction": "7.1x (Table 4, fp32 baseline, 'CUDA')",
                           "kv_fetch_speedup": "1.96x Triton vs PyTorch fetch_unpacked, 143 tokens, "
                                               "NVIDIA GPU on Colab, model and precision unstated (Table 6)"},
     }
     print(json.dumps(line))
+
+
+def fp16_attention_baseline(torch, units, n_ctx, replica_bytes, K):
+    """Plain decode attention over an unquantized fp16 cache of the same shape
+    (one query per (layer, head) unit, n_ctx cached keys and values of 64
+    fp16 each, 256 B per token-head against the packed cache's 72 B), with
+    PyTorch on the same GPU: scaled_dot_product_attention, and an explicit
+    matmul - softmax (fp32) - matmul. Replicas rotate as for the fused path so
+    each call reads HBM. Context for the fused kernel, not part of the path."""
+    import torch.nn.functional as F
+    dev = torch.device("cuda:0")
+    per = units * n_ctx * 64 * 2 * 2
+    R = max(2, math.ceil(replica_bytes / per))
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    kv = [(torch.randn((1, units, n_ctx, 64), generator=g, device=dev, dtype=torch.float16),
+           torch.randn((1, units, n_ctx, 64), generator=g, device=dev, dtype=torch.float16)) for _ in range(R)]
+    q = torch.randn((1, units, 1, 64), generator=g, device=dev, dtype=torch.float16)
+
+    def sdpa(r):
+        return F.scaled_dot_product_attention(q, kv[r][0], kv[r][1])
+
+    def explicit(r):
+        k, v = kv[r]
+        w = torch.softmax(torch.matmul(k[0], q[0].transpose(1, 2).contiguous()).float() * 0.125, dim=1)
+        return torch.matmul(w.transpose(1, 2).to(torch.float16).contiguous(), v[0])
+
+    out = {"units": units, "tokens": n_ctx, "kv_bytes_per_call": units * n_ctx * 256, "replicas": R}
+    for name, fn in (("sdpa", sdpa), ("matmul_softmax", explicit)):
+        for r in range(R):
+            fn(r)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for s in range(K):
+            fn(s % R)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / K
+        out[name + "_ms"] = round(ms, 5)
+        out[name + "_kv_gbs"] = round(units * n_ctx * 256 / (ms * 1e-3) / 1e9, 1)
+    del kv
+    torch.cuda.empty_cache()
+    return out
 
 
 def measured_traffic(workload):
