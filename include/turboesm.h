@@ -66,6 +66,7 @@ typedef int32_t tq_status;
 #define TQ_ERR_ARG       -1  /* null pointer, bad count or unknown flag      */
 #define TQ_ERR_DIM       -2  /* head_dim != 64 or layer range outside [0, L) */
 #define TQ_ERR_ALIGN     -3  /* a pointer misses its documented alignment    */
+#define TQ_ERR_LUT_ORDER -4  /* a host table is not strictly ascending       */
 #define TQ_ERR_CAPACITY  -5  /* slots not a positive multiple of 64, or a
                                 workspace smaller than required              */
 #define TQ_ERR_HIP       -6  /* a HIP runtime call or kernel launch failed   */
@@ -250,6 +251,26 @@ TQ_API size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B,
  */
 TQ_API tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal,
                                 float* pi_out, float* sing_out, void* stream);
+
+/* Calibrated 8-level table per head (Sec. 3.3: calibrated tables, separate
+ * for K and V; Eq. 5 fitted to data): the 1-D Lloyd iteration (k-means) on
+ * every normalized coordinate u = 8 x^ / ||x^|| of the head's calibration
+ * vectors, x^ = Pi x in fp64 (x^ = x when pi is NULL; a zero vector gives
+ * zeros, as in the quantizer). Each iteration assigns u to level
+ * #{m : u > (c_m + c_{m+1})/2}, replaces every level by the mean of its cell
+ * (fp64 sums; an empty cell keeps its level), sorts the levels and stops
+ * once the largest level change is below tol, or after max_iter iterations.
+ *   x        device [nheads][ncal][64] fp32: post-RoPE keys for the K table,
+ *            values for the V table.
+ *   pi       device [nheads][64][64] fp32 rotations, or NULL.
+ *   init     HOST [8] fp32 starting levels, strictly ascending (for example
+ *            the Gaussian Lloyd-Max table).
+ *   max_iter >= 1;  tol >= 0 (finite).
+ *   lut_out  device [nheads][8] fp32, ascending.
+ */
+TQ_API tq_status tq_calibrate_lut(const float* x, int32_t nheads, int32_t ncal, const float* pi,
+                           const float* init, int32_t max_iter, double tol, float* lut_out,
+                           void* stream);
 
 /* Message of the last failing call on this thread ("" if none). */
 TQ_API const char* tq_last_error(void);

@@ -277,6 +277,23 @@ def kmeans_1d(samples, init, max_iter: int = 100, tol: float = 1e-7):
     return c
 
 
+def normalized_coordinates(x, pi=None) -> np.ndarray:
+    """The coordinates a table quantizes: u = 8 x^ / ||x^|| with x^ = Pi x in
+    fp64 (x^ = x when pi is None); a zero vector gives zeros, as the
+    quantizer's inv = 0 does. x: [n][64]. Returns [n][64] float64."""
+    X = np.asarray(x, dtype=np.float64).reshape(-1, D)
+    xh = X if pi is None else X @ np.asarray(pi, dtype=np.float64).T
+    n = np.sqrt(np.sum(xh * xh, axis=1, keepdims=True))
+    return np.where(n > 0, xh * (8.0 / np.where(n > 0, n, 1.0)), 0.0)
+
+
+def calibrate_lut(x, pi, init, max_iter: int = 100, tol: float = 1e-7) -> np.ndarray:
+    """Calibrated 8-level table of one head (Sec. 3.3, calibrated LUTs): the
+    1-D Lloyd iteration of kmeans_1d on every normalized coordinate of the
+    calibration vectors x [n][64] (rotated by pi unless None)."""
+    return kmeans_1d(normalized_coordinates(x, pi).reshape(-1), init, max_iter, tol)
+
+
 # --------------------------------------------------------------------------
 # Head-wise SVD calibration (Sec. 3.2)
 # --------------------------------------------------------------------------

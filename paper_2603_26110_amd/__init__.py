@@ -7,7 +7,7 @@ raise ``RuntimeError`` (there is no fallback path).
 
 Entry points (same names as the C ABI without the ``tq_`` prefix):
     rope_table, quantize_pack, decode_attend, decode_step,
-    decode_workspace_bytes, calibrate_rotation, cache_bytes, last_error, version
+    decode_workspace_bytes, calibrate_rotation, calibrate_lut, cache_bytes, last_error, version
 """
 from __future__ import annotations
 
@@ -19,7 +19,7 @@ import torch
 
 __all__ = [
     "Params", "Cache", "TQError", "rope_table", "quantize_pack", "decode_attend", "decode_step",
-    "decode_workspace_bytes", "calibrate_rotation", "cache_bytes", "last_error", "version",
+    "decode_workspace_bytes", "calibrate_rotation", "calibrate_lut", "cache_bytes", "last_error", "version",
     "V_ROTATE", "V_QJL", "QJL_PAPER", "ROPE_HALF", "INPUT_ROTATED", "OUT_FP32", "lib_path",
 ]
 
@@ -73,6 +73,8 @@ def _load():
     L.tq_decode_workspace_bytes.argtypes = [P, i32, i32, i32]
     L.tq_decode_workspace_bytes.restype = sz
     L.tq_calibrate_rotation.argtypes = [P, i32, i32, P, P, P]
+    L.tq_calibrate_lut.argtypes = [P, i32, i32, P, P, i32, ctypes.c_double, P, P]
+    L.tq_calibrate_lut.restype = i32
     L.tq_calibrate_rotation.restype = i32
     _lib = L
     return L
@@ -253,6 +255,29 @@ def decode_step(params: Params, cache: Cache, q, k, v, pos, seq_slot0, seq_len, 
                             _ptr(pos), _ptr(seq_slot0), _ptr(seq_len), int(max_len), _ptr(pi),
                             _ptr(lut_k), _ptr(lut_v), _ptr(qjl_s), _ptr(ebar), _ptr(out),
                             _ptr(workspace), wsz, _stream(q.device)))
+    return out
+
+
+def calibrate_lut(x: torch.Tensor, pi=None, init=None, max_iter: int = 100,
+                  tol: float = 1e-7) -> torch.Tensor:
+    """x: [nheads][ncal][64] fp32 calibration vectors (post-RoPE keys or values),
+    pi: [nheads][64][64] rotations or None, init: 8 ascending starting levels
+    (default: the Gaussian 8-level table). Returns the tables [nheads][8]."""
+    L = _load()
+    _dev(x, "x", torch.float32)
+    if x.dim() != 3 or x.shape[-1] != 64:
+        raise ValueError("x must be [nheads][ncal][64]")
+    nh, ncal = x.shape[:2]
+    if pi is not None:
+        _dev(pi, "pi", torch.float32)
+        if tuple(pi.shape) != (nh, 64, 64):
+            raise ValueError("pi must be [nheads][64][64]")
+    from .synth import GAUSS_LEVELS_MAX1960
+    init_h = (GAUSS_LEVELS_MAX1960 if init is None else init)
+    init_arr = (ctypes.c_float * 8)(*[float(v) for v in init_h])
+    out = torch.empty((nh, 8), dtype=torch.float32, device=x.device)
+    _check(L.tq_calibrate_lut(_ptr(x), nh, ncal, _ptr(pi), ctypes.cast(init_arr, ctypes.c_void_p),
+                              int(max_iter), float(tol), _ptr(out), _stream(x.device)))
     return out
 
 

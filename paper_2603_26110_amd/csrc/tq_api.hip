@@ -236,4 +236,24 @@ tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal, fl
                     "tq_calibrate_rotation launch");
 }
 
+tq_status tq_calibrate_lut(const float* x, int32_t nheads, int32_t ncal, const float* pi,
+                           const float* init, int32_t max_iter, double tol, float* lut_out,
+                           void* stream) {
+  if (nheads < 0 || ncal < 0) return fail(TQ_ERR_ARG, "nheads and ncal must be >= 0");
+  if (!init) return fail(TQ_ERR_ARG, "init must not be NULL");
+  for (int m = 0; m < 8; ++m)
+    if (!std::isfinite(init[m])) return fail(TQ_ERR_ARG, "init levels must be finite");
+  for (int m = 0; m < 7; ++m)
+    if (!(init[m] < init[m + 1])) return fail(TQ_ERR_LUT_ORDER, "init levels must be strictly ascending");
+  if (max_iter < 1) return fail(TQ_ERR_ARG, "max_iter must be >= 1");
+  if (!(tol >= 0.0) || !std::isfinite(tol)) return fail(TQ_ERR_ARG, "tol must be finite and >= 0");
+  if (nheads == 0) return ok();
+  if (!x || !lut_out) return fail(TQ_ERR_ARG, "x and lut_out must not be NULL");
+  if (ncal == 0) return fail(TQ_ERR_ARG, "ncal must be positive");
+  if (nheads > 65535 * 1024) return fail(TQ_ERR_ARG, "too many heads");
+  return hip_status(tq::launch_calibrate_lut(x, nheads, ncal, pi, init, max_iter, tol, lut_out,
+                                             (hipStream_t)stream),
+                    "tq_calibrate_lut launch");
+}
+
 }  // extern "C"

@@ -165,4 +165,136 @@ hipError_t launch_calibrate(const float* x, int nheads, int ncal, float* pi_out,
   return hipGetLastError();
 }
 
+// ------------------------------------------------------- table calibration
+// Calibrated 8-level table per head (Sec. 3.3: calibrated, separate K and V
+// tables): the 1-D Lloyd iteration (k-means) on every normalized coordinate
+// u = 8 x^ / ||x^|| (x^ = Pi x in fp64, x^ = x without Pi; a zero vector
+// gives zeros) of the head's calibration vectors. Per iteration: assign each
+// u to the level whose midpoint interval holds it (u > t_m strictly counts,
+// so a tie goes to the lower level), replace each level by the mean of its
+// cell (fp64 sums; an empty cell keeps its level), take the largest level
+// change, sort, and stop once that change is below tol, or after max_iter.
+//
+// One block of 4 waves per head. u is recomputed every iteration (no
+// workspace): a wave takes one vector at a time, lane i forming x^_i from
+// row i of Pi staged in LDS and the vector staged in LDS, the norm by a wave
+// reduction. Every lane owns 8 fp64 bins and counts in LDS; the block sums
+// them in a fixed order.
+constexpr int kLutWaves = 4;
+constexpr int kPiPitch = kDim + 1;       // doubles per staged row of Pi
+
+struct LutSmem {
+  double pi[kDim * kPiPitch];
+  double xv[kLutWaves][kDim];
+  double bsum[kLutWaves * kDim][8];
+  int bcnt[kLutWaves * kDim][8];
+  double psum[32][8];
+  int pcnt[32][8];
+  double c[8];
+  int done;
+};
+
+__device__ __forceinline__ double wave_sum_f64(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void calibrate_lut_kernel(const float* x, int ncal, const float* pi,
+                                                            LutInit init, int max_iter, double tol,
+                                                            float* lut_out) {
+  __shared__ LutSmem sm;
+  const int head = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float* X = x + (int64_t)head * ncal * kDim;
+  const bool rot = pi != nullptr;
+  if (rot) {
+    const float* P = pi + (int64_t)head * kDim * kDim;
+    for (int e = t; e < kDim * kDim; e += 256) sm.pi[(e >> 6) * kPiPitch + (e & 63)] = (double)P[e];
+  }
+  if (t < 8) sm.c[t] = (double)init.c[t];
+  if (t == 0) sm.done = 0;
+  __syncthreads();
+  double* bs = sm.bsum[wave * kDim + lane];
+  int* bc = sm.bcnt[wave * kDim + lane];
+  for (int it = 0; it < max_iter; ++it) {
+    double th[7];
+#pragma unroll
+    for (int m = 0; m < 7; ++m) th[m] = 0.5 * (sm.c[m] + sm.c[m + 1]);
+#pragma unroll
+    for (int m = 0; m < 8; ++m) { bs[m] = 0.0; bc[m] = 0; }
+    for (int v = wave; v < ncal; v += kLutWaves) {
+      const double xi = (double)X[(int64_t)v * kDim + lane];
+      double xh = xi;
+      if (rot) {
+        sm.xv[wave][lane] = xi;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        const double* row = sm.pi + lane * kPiPitch;
+        xh = 0.0;
+#pragma unroll 8
+        for (int k = 0; k < kDim; ++k) xh = fma(row[k], sm.xv[wave][k], xh);
+      }
+      const double n2 = wave_sum_f64(xh * xh);
+      const double u = (n2 > 0.0) ? xh * (8.0 / sqrt(n2)) : 0.0;
+      int m = 0;
+#pragma unroll
+      for (int k = 0; k < 7; ++k) m += (u > th[k]) ? 1 : 0;
+      bs[m] += u;
+      bc[m] += 1;
+      if (rot) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // xv is rewritten next
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      }
+    }
+    __syncthreads();
+    {
+      // 32 partials per level: thread (part, m) sums 8 lanes' bins in order
+      const int m = t & 7, part = t >> 3;
+      double sacc = 0.0;
+      int cacc = 0;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        sacc += sm.bsum[part * 8 + r][m];
+        cacc += sm.bcnt[part * 8 + r][m];
+      }
+      sm.psum[part][m] = sacc;
+      sm.pcnt[part][m] = cacc;
+    }
+    __syncthreads();
+    if (t == 0) {
+      double cn[8], delta = 0.0;
+      for (int m = 0; m < 8; ++m) {
+        double sacc = 0.0;
+        int cacc = 0;
+        for (int part = 0; part < 32; ++part) { sacc += sm.psum[part][m]; cacc += sm.pcnt[part][m]; }
+        cn[m] = (cacc > 0) ? sacc / (double)cacc : sm.c[m];
+        delta = fmax(delta, fabs(cn[m] - sm.c[m]));
+      }
+      for (int i = 1; i < 8; ++i) {          // insertion sort, ascending
+        const double key = cn[i];
+        int j = i - 1;
+        while (j >= 0 && cn[j] > key) { cn[j + 1] = cn[j]; --j; }
+        cn[j + 1] = key;
+      }
+      for (int m = 0; m < 8; ++m) sm.c[m] = cn[m];
+      sm.done = (delta < tol) ? 1 : 0;
+    }
+    __syncthreads();
+    if (sm.done) break;
+  }
+  if (t < 8) lut_out[(int64_t)head * 8 + t] = (float)sm.c[t];
+}
+
+hipError_t launch_calibrate_lut(const float* x, int nheads, int ncal, const float* pi, const float* init,
+                                int max_iter, double tol, float* lut_out, hipStream_t st) {
+  LutInit in;
+  for (int m = 0; m < 8; ++m) in.c[m] = init[m];
+  hipLaunchKernelGGL(calibrate_lut_kernel, dim3(nheads), dim3(256), 0, st, x, ncal, pi, in, max_iter, tol,
+                     lut_out);
+  return hipGetLastError();
+}
+
 }  // namespace tq

@@ -72,6 +72,12 @@ hipError_t launch_rope_table(float* cs, int positions, double base, hipStream_t 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t st);
 void decode_plan(int units, int max_len, int* waves, int* nsplit, int* split_tiles);
 hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st);
+// Initial levels of the table calibration (by value: a host array).
+struct LutInit {
+  float c[8];
+};
+hipError_t launch_calibrate_lut(const float* x, int nheads, int ncal, const float* pi, const float* init,
+                                int max_iter, double tol, float* lut_out, hipStream_t st);
 hipError_t launch_calibrate(const float* x, int nheads, int ncal, float* pi_out,
                             float* sing_out, hipStream_t st);
 

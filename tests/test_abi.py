@@ -38,7 +38,8 @@ def _defines():
 def test_header_declares_the_entry_points():
     assert _declared_functions() == sorted([
         "tq_cache_bytes", "tq_rope_table", "tq_quantize_pack", "tq_decode_attend", "tq_decode_step",
-        "tq_decode_workspace_bytes", "tq_calibrate_rotation", "tq_last_error", "tq_version"])
+        "tq_decode_workspace_bytes", "tq_calibrate_rotation", "tq_calibrate_lut", "tq_last_error",
+        "tq_version"])
 
 
 def test_library_exports_exactly_the_declared_symbols():
@@ -211,3 +212,24 @@ def test_decode_step_argument_checks():
     assert _step(_params(), _cache(), kv=FAKE + 4) == -3
     assert _step(_params(), _cache(), max_len=129) == -5
     assert _step(_params(), _cache(), B=0) == 0
+
+
+def test_calibrate_lut_argument_checks():
+    L = tq._load()
+    P = ctypes.c_void_p
+    good = (ctypes.c_float * 8)(-2.0, -1.3, -0.75, -0.25, 0.25, 0.75, 1.3, 2.0)
+    flat = (ctypes.c_float * 8)(0.0, 0.0, -0.75, -0.25, 0.25, 0.75, 1.3, 2.0)
+    nan = (ctypes.c_float * 8)(float("nan"), -1.3, -0.75, -0.25, 0.25, 0.75, 1.3, 2.0)
+    c = lambda init, nh=2, ncal=10, it=100, tol=1e-7, x=FAKE, out=FAKE: L.tq_calibrate_lut(
+        P(x) if x else None, nh, ncal, None, ctypes.cast(init, P) if init is not None else None, it, tol,
+        P(out) if out else None, None)
+    assert c(None) == -1 and "init" in tq.last_error()
+    assert c(flat) == -4 and "ascending" in tq.last_error()
+    assert c(nan) == -1 and "finite" in tq.last_error()
+    assert c(good, it=0) == -1
+    assert c(good, tol=-1.0) == -1
+    assert c(good, tol=float("inf")) == -1
+    assert c(good, nh=-1) == -1
+    assert c(good, ncal=0) == -1
+    assert c(good, x=0) == -1
+    assert c(good, nh=0) == 0 and tq.last_error() == ""

@@ -286,3 +286,35 @@ def test_calibrate_rotation_matches_svd():
                          np.abs(np.diff(np.concatenate((ref_s, [-np.inf])))))
         sep = gap > 1e-3 * ref_s[0]
         np.testing.assert_allclose(P[sep], ref_pi[sep].astype(np.float64), atol=1e-4)
+
+
+# ---------------------------------------------------------- table calibration
+@pytest.mark.parametrize("kind,rotate", [("k", True), ("v", True), ("v", False)])
+def test_calibrate_lut_matches_oracle(kind, rotate):
+    g = synth.rng(41)
+    H, ncal = 3, 1024
+    ch = synth.outlier_channels(g, 1, H)
+    if kind == "k":
+        x = synth.keys(g, 1, 1, ncal, H, ch)[0, 0].transpose(1, 0, 2).copy()      # [H][ncal][64]
+    else:
+        x = synth.values(g, 1, 1, ncal, H)[0, 0].transpose(1, 0, 2).copy()
+    x[0, 5] = 0.0                                                               # a zero vector
+    pi = synth.rotations(g, 1, H)[0]
+    init = GAUSS_LUT
+    got = tq.calibrate_lut(torch.from_numpy(x).cuda(), torch.from_numpy(pi).cuda() if rotate else None,
+                           init).cpu().numpy()
+    for h in range(H):
+        ref = oracle.calibrate_lut(x[h], pi[h] if rotate else None, init)
+        np.testing.assert_allclose(got[h], ref, rtol=0, atol=2e-6)
+        assert np.all(np.diff(got[h]) > 0)
+
+
+def test_calibrate_lut_keeps_empty_cells_and_stops_at_max_iter():
+    g = synth.rng(42)
+    x = g.standard_normal((2, 256, 64)).astype(np.float32)
+    init = np.array([-40.0, -1.3, -0.75, -0.25, 0.25, 0.75, 1.3, 40.0], np.float32)   # outer cells stay empty
+    got = tq.calibrate_lut(torch.from_numpy(x).cuda(), None, init, max_iter=3).cpu().numpy()
+    for h in range(2):
+        ref = oracle.calibrate_lut(x[h], None, init, max_iter=3)
+        np.testing.assert_allclose(got[h], ref, rtol=0, atol=2e-6)
+        assert got[h][0] == -40.0 and got[h][-1] == 40.0

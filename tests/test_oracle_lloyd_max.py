@@ -114,3 +114,40 @@ def test_lloyd_max_iteration_is_a_fixed_point(levels):
     cn = (norm.pdf(edges[:-1]) - norm.pdf(edges[1:])) / mass
     assert np.max(np.abs(cn - c)) < 1e-13
     assert np.all(np.diff(c) > 0)
+
+
+# ---- calibrated tables: normalized coordinates and the per-head Lloyd fit
+def test_normalized_coordinates_have_norm_8_and_the_rotated_direction():
+    g = np.random.Generator(np.random.PCG64(21))
+    x = g.standard_normal((50, 64)) * np.exp(g.standard_normal((50, 1)))
+    q, _ = np.linalg.qr(g.standard_normal((64, 64)))
+    u = oracle.normalized_coordinates(x, q)
+    np.testing.assert_allclose(np.linalg.norm(u, axis=1), 8.0, rtol=1e-14)
+    xh = x @ q.T
+    cos = np.sum(u * xh, axis=1) / (8.0 * np.linalg.norm(xh, axis=1))
+    np.testing.assert_allclose(cos, 1.0, rtol=1e-14)
+    z = oracle.normalized_coordinates(np.zeros((2, 64)), q)
+    assert np.all(z == 0.0)
+    # no rotation: the unit vector of x itself, times 8
+    np.testing.assert_allclose(oracle.normalized_coordinates(x, None),
+                               8.0 * x / np.linalg.norm(x, axis=1, keepdims=True), rtol=1e-14)
+
+
+def test_calibrated_table_of_isotropic_vectors_fits_the_exact_marginal():
+    # For isotropic vectors in 64 dimensions (any rotation), a normalized
+    # coordinate is u = 8 t with t the coordinate of a uniform unit vector:
+    # t^2 ~ Beta(1/2, 63/2), symmetric sign. The table calibrated on the
+    # vectors must match the Lloyd fit of samples drawn from that law directly
+    # (a wrong scale, a missing rotation or a norm of the unrotated vector
+    # would all move it).
+    g = np.random.Generator(np.random.PCG64(22))
+    x = g.standard_normal((20000, 64))
+    q, _ = np.linalg.qr(g.standard_normal((64, 64)))
+    ref, _, _ = oracle.lloyd_max_gaussian(8)
+    c = oracle.calibrate_lut(x, q, ref)
+    t = np.sqrt(g.beta(0.5, 31.5, 2_000_000)) * np.where(g.random(2_000_000) < 0.5, -1.0, 1.0)
+    c_law = oracle.kmeans_1d(8.0 * t, ref)
+    assert np.all(np.diff(c) > 0)
+    assert np.max(np.abs(c - c_law)) < 0.01, np.abs(c - c_law)
+    # lighter tails than N(0, 1): the outer levels sit inside the Gaussian ones
+    assert c[-1] < ref[-1] and c[0] > ref[0]
