@@ -1,6 +1,7 @@
 """Shared helpers of the GPU parity tests: seeded inputs for both sides,
-running the library through its C ABI, and bringing the device cache back
-for the oracle."""
+running the library through its C ABI, moving the oracle's cache to the
+device, and reading the device cache back for comparison with the oracle's
+(never as an oracle input)."""
 from __future__ import annotations
 
 import numpy as np
@@ -92,6 +93,16 @@ class Case:
                              np.asarray(self.q, np.float32), q_pos, seq_slot0, seq_len, self.pi,
                              self.lut_k, self.lut_v, self.S, ebar=self.ebar, layer0=self.layer0,
                              units=units)
+
+
+def to_gpu(oc: oracle.Cache) -> tq.Cache:
+    """A device cache holding the bytes the oracle's quantizer wrote (so that
+    decode parity never feeds GPU output to the oracle)."""
+    cache = tq.Cache(oc.L, oc.H, oc.slots)
+    cache.k_codes.copy_(torch.from_numpy(oc.k))
+    cache.v_codes.copy_(torch.from_numpy(oc.v))
+    cache.scalars.copy_(torch.from_numpy(oc.s.view(np.int16)))
+    return cache
 
 
 def to_oracle(cache: tq.Cache) -> oracle.Cache:

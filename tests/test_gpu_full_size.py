@@ -8,12 +8,14 @@ kernel reads the whole packed cache).
                           tile-aligned packed offsets
   ESM-2 3B shape          36 layers x 40 heads, batch 16, 8192 cached tokens
 
-The oracle recomputes a sample of (layer, sequence, head) units one by one
-from the cache bytes the GPU wrote (fp64 decode, 2e-3 on fp32 output and
-max(2e-3, 1 fp16 ulp) on the fp16 output); the codes of sampled tokens,
-including the appended one, are checked against the oracle's quantizer of the
-same inputs: equal, or one level apart where the rotated coordinate lies
-within rounding of a threshold."""
+For a sample of (layer, sequence, head) units the oracle quantizes that
+unit's raw tokens (the cached ones and the new one) into a cache of its own
+and decodes there in fp64: 2e-3 on the fp32 output and max(2e-3, 1 fp16 ulp)
+on the fp16 output. The GPU's codes of sampled tokens, including the appended
+one, are checked against the oracle's quantizer of the same inputs: equal, or
+one level apart where the rotated coordinate lies within rounding of a
+threshold; its norms of every token of a sampled unit within one fp16 ulp of
+the oracle's."""
 import numpy as np
 import pytest
 import torch
@@ -37,10 +39,11 @@ def _i64(x):
     return torch.tensor(np.asarray(x, np.int64), dtype=torch.int64).cuda()
 
 
-def _unit_cache(cache, l, h, s0, n):
-    """Oracle cache of one (layer, head) region: slots [s0, s0 + cap) of the
-    GPU cache, cap = n rounded up to a tile (s0 is tile-aligned, so tile
-    layouts are unchanged by the shift)."""
+def _gpu_region(cache, l, h, s0, n):
+    """The GPU's bytes of slots [s0, s0 + cap) of one (layer, head) region as
+    a one-head oracle.Cache layout, cap = n rounded up to a tile (s0 is
+    tile-aligned, so tile layouts are unchanged by the shift). Compared with
+    the oracle's bytes, never given to the oracle."""
     cap = (n + 63) // 64 * 64
     oc = oracle.Cache(1, 1, cap)
     base = (l * cache.num_heads + h) * cache.slots + s0
@@ -50,15 +53,34 @@ def _unit_cache(cache, l, h, s0, n):
     return oc
 
 
-def _check_units(cache, units, out16, out32, q, pos, offs, n_att, pi, lut_k, lut_v, S, flags, cs_host):
-    """units: (l, b, h) triples; q [L][B][H][64] host float32; n_att[b] tokens attended."""
+def _oracle_unit_cache(krows, vrows, l, h, pi, lut_k, lut_v, S, flags, cs_host):
+    """The oracle's own cache of one unit: its raw tokens krows/vrows [n][64]
+    (token j at position j) quantized into slots 0 .. n-1."""
+    n = krows.shape[0]
+    oc = oracle.Cache(1, 1, (n + 63) // 64 * 64)
+    oracle.quantize_pack(oc, flags, cs_host, krows.reshape(1, 1, n, 1, 64), vrows.reshape(1, 1, n, 1, 64),
+                         [0], [0], pi[l, h][None, None], lut_k[l, h][None, None], lut_v[l, h][None, None], S)
+    return oc
+
+
+def _check_units(cache, units, raw, out16, out32, q, pos, offs, n_att, pi, lut_k, lut_v, S, flags, cs_host):
+    """units: (l, b, h) triples; raw[(l, b, h)] = (k rows, v rows) [n_att[b]][64]
+    host float32; q [L][B][H][64] host float32; n_att[b] tokens attended."""
     worst = 0.0
     for (l, b, h) in units:
         n = int(n_att[b])
-        oc = _unit_cache(cache, l, h, int(offs[b]), n)
-        # every attended token was written (a skipped append or prefill would
-        # leave zero norms, which both sides would then agree on)
-        assert np.all(oc.scalars(0, 0)[:n, 0] != 0) and np.all(oc.scalars(0, 0)[:n, 2] != 0), (l, b, h)
+        krows, vrows = raw[(l, b, h)]
+        assert krows.shape[0] == n
+        oc = _oracle_unit_cache(krows, vrows, l, h, pi, lut_k, lut_v, S, flags, cs_host)
+        # the GPU wrote every attended token (a skipped append or prefill
+        # leaves zero norms), and its norms agree with the oracle's
+        gs = _gpu_region(cache, l, h, int(offs[b]), n).scalars(0, 0)[:n]
+        os_ = oc.scalars(0, 0)[:n]
+        assert np.all(gs[:, 0] != 0) and np.all(gs[:, 2] != 0), (l, b, h)
+        for col in (0, 2):
+            ng = gs[:, col].view(np.float16).astype(np.float64)
+            no = os_[:, col].view(np.float16).astype(np.float64)
+            assert np.all(np.abs(ng - no) <= fp16_ulp(no) + 1e-12), (l, b, h, col)
         ref = oracle.decode(oc, flags, cs_host, q[l, b, h].reshape(1, 1, 1, 64), [int(pos[b])], [0], [n],
                             pi[l, h][None, None], lut_k[l, h][None, None], lut_v[l, h][None, None],
                             S)[0, 0, 0]
@@ -77,7 +99,7 @@ def _check_codes(cache, samples, cs_host, pi, lut_k, lut_v, S, flags):
     token; compares the GPU's key and value codes and norms with the oracle's
     quantizer of the same inputs."""
     for (l, h, slot, pos, krow, vrow) in samples:
-        oc = _unit_cache(cache, l, h, slot - slot % 64, slot % 64 + 1)
+        oc = _gpu_region(cache, l, h, slot - slot % 64, slot % 64 + 1)
         r = slot % 64
         for is_key, which, x, lut, col in ((True, "k", krow, lut_k, 0), (False, "v", vrow, lut_v, 2)):
             xh = oracle.rotated_input(np.asarray(x, np.float32), is_key, pos, cs_host, pi[l, h],
@@ -145,8 +167,10 @@ def test_full_650m_33layer_step():
                                       T + 1, pi_d, lk_d, lv_d, S_d)
     assert np.all(np.isfinite(out32))
     units = _sample_units(synth.rng(1), L, 1, H, 24)
-    _check_units(cache, units, out16, out32, q.astype(np.float32), [T], [0], [T + 1], pi, lut_k, lut_v, S,
-                 tq.V_ROTATE, cs_host)
+    raw = {(l, b, h): (k[l, b, :T + 1, h].astype(np.float32), v[l, b, :T + 1, h].astype(np.float32))
+           for (l, b, h) in units}
+    _check_units(cache, units, raw, out16, out32, q.astype(np.float32), [T], [0], [T + 1], pi, lut_k, lut_v,
+                 S, tq.V_ROTATE, cs_host)
     samples = [(l, h, j, j, k[l, 0, j, h], v[l, 0, j, h])
                for (l, _, h) in units[:8] for j in (0, 63, 64, 777, T - 1, T)]
     _check_codes(cache, samples, cs_host, pi, lut_k, lut_v, S, tq.V_ROTATE)
@@ -175,6 +199,7 @@ def test_full_ragged_b64_step():
     k_new = torch.empty_like(q_d)
     v_new = torch.empty_like(q_d)
     samples = []
+    raw = {}
     for l in range(L):
         gen = synth.device_generator(wl.seed, l, "cuda")
         kl = synth.keys_on(gen, B, int(lens.max()) + 1, H, ch[l], torch.float16, "cuda")
@@ -189,6 +214,8 @@ def test_full_ragged_b64_step():
             v_new[l, b] = vl[b, n]
         for (ul, ub, uh) in units:
             if ul == l:
+                n = int(lens[ub]) + 1
+                raw[(ul, ub, uh)] = (kl[ub, :n, uh].float().cpu().numpy(), vl[ub, :n, uh].float().cpu().numpy())
                 for j in (0, int(lens[ub]) - 1):
                     samples.append((l, uh, int(offs[ub]) + j, j, kl[ub, j, uh].float().cpu().numpy(),
                                     vl[ub, j, uh].float().cpu().numpy()))
@@ -197,8 +224,8 @@ def test_full_ragged_b64_step():
                                       pi_d, lk_d, lv_d, S_d)
     assert np.all(np.isfinite(out32))
     q_host = q_d.float().cpu().numpy()
-    _check_units(cache, units, out16, out32, q_host, lens, offs, lens + 1, pi, lut_k, lut_v, S, tq.V_ROTATE,
-                 cs_host)
+    _check_units(cache, units, raw, out16, out32, q_host, lens, offs, lens + 1, pi, lut_k, lut_v, S,
+                 tq.V_ROTATE, cs_host)
     kn, vn = k_new.float().cpu().numpy(), v_new.float().cpu().numpy()
     samples += [(l, h, int(offs[b]) + int(lens[b]), int(lens[b]), kn[l, b, h], vn[l, b, h])
                 for (l, b, h) in units[:8]]
@@ -230,6 +257,7 @@ def test_full_3b_step():
     zeros = _i32(np.zeros(B))
     offs_d = _i64(offs)
     samples = []
+    raw = {}
     for l in range(L):
         gen = synth.device_generator(wl.seed, l, "cuda")
         kl = synth.keys_on(gen, B, T + 1, H, ch[l], torch.float16, "cuda")
@@ -241,6 +269,8 @@ def test_full_3b_step():
         v_new[l] = vl[:, T]
         for (ul, ub, uh) in units:
             if ul == l:
+                raw[(ul, ub, uh)] = (kl[ub, :T + 1, uh].float().cpu().numpy(),
+                                     vl[ub, :T + 1, uh].float().cpu().numpy())
                 for j in (0, 4095, T - 1):
                     samples.append((l, uh, int(offs[ub]) + j, j, kl[ub, j, uh].float().cpu().numpy(),
                                     vl[ub, j, uh].float().cpu().numpy()))
@@ -250,8 +280,8 @@ def test_full_3b_step():
                                       lv_d, S_d)
     assert np.all(np.isfinite(out32))
     q_host = q_d.float().cpu().numpy()
-    _check_units(cache, units, out16, out32, q_host, lens, offs, lens + 1, pi, lut_k, lut_v, S, tq.V_ROTATE,
-                 cs_host)
+    _check_units(cache, units, raw, out16, out32, q_host, lens, offs, lens + 1, pi, lut_k, lut_v, S,
+                 tq.V_ROTATE, cs_host)
     kn, vn = k_new.float().cpu().numpy(), v_new.float().cpu().numpy()
     samples += [(l, h, int(offs[b]) + T, T, kn[l, b, h], vn[l, b, h]) for (l, b, h) in units]
     _check_codes(cache, samples, cs_host, pi, lut_k, lut_v, S, tq.V_ROTATE)

@@ -6,15 +6,17 @@ T < 64 one wave per vector), ragged and unaligned slots, every sign mode.
 End to end (raw keys/values, GPU RoPE and rotation in binary32): codes may
 differ only where the oracle's fp64 coordinate sits within rounding of a
 decision threshold.
-Decode: GPU output against the fp64 oracle run on the very cache bytes the
-GPU wrote, |err| <= 2e-3 (fp32 output), fp16 output within max(2e-3, 1 ulp).
+Decode: the GPU decodes an upload of the cache the oracle's quantizer wrote
+and the oracle decodes that cache in fp64 (or, end to end, each side
+quantizes the same inputs into a cache of its own), |err| <= 2e-3 (fp32
+output), fp16 output within max(2e-3, 1 ulp).
 """
 import numpy as np
 import pytest
 import torch
 
 import paper_2603_26110_amd as tq
-from gpu_cases import Case, GAUSS_LUT, fp16_ulp, to_oracle
+from gpu_cases import Case, GAUSS_LUT, fp16_ulp, to_gpu, to_oracle
 from oracle import oracle
 from paper_2603_26110_amd import synth
 
@@ -152,32 +154,45 @@ def test_quantize_end_to_end_matches_up_to_threshold_rounding(T):
 
 
 # --------------------------------------------------------------------- decode
-def _decode_check(case, cache, q_pos, seq_slot0, seq_len, max_len, flags=None):
-    flags = case.flags if flags is None else flags
-    out32 = case.gpu_decode(cache, q_pos, seq_slot0, seq_len, max_len, flags=flags | tq.OUT_FP32)
-    torch.cuda.synchronize()
-    ref = case.oracle_decode(to_oracle(cache), q_pos, seq_slot0, seq_len, flags=flags)
-    got = out32.cpu().numpy().astype(np.float64)
+# Decode parity takes the cache from the oracle's quantizer: the GPU decodes
+# an upload of those bytes and the oracle decodes its own cache, so no GPU
+# output ever reaches the oracle. test_decode_steps_append_then_attend runs
+# both sides end to end instead (each quantizes the same inputs).
+def _compare(case, got32, got16, ref):
+    got = got32.astype(np.float64)
     err = np.abs(got - ref)
     assert np.all(np.isfinite(got) == np.isfinite(ref))
     fin = np.isfinite(ref)
     assert np.max(err[fin], initial=0.0) <= TOL, np.max(err[fin])
-    if case.io == "f16":
-        out16 = case.gpu_decode(cache, q_pos, seq_slot0, seq_len, max_len, flags=flags)
-        torch.cuda.synchronize()
-        g16 = out16.cpu().numpy().astype(np.float64)
+    if got16 is not None:
+        g16 = got16.astype(np.float64)
         r16 = ref.astype(np.float16).astype(np.float64)
         lim = np.maximum(TOL, fp16_ulp(r16))
         assert np.all(np.abs(g16 - r16)[fin] <= lim[fin])
-    return got, ref
+    return got
+
+
+def _decode_check(case, oc, q_pos, seq_slot0, seq_len, max_len, flags=None):
+    flags = case.flags if flags is None else flags
+    cache = to_gpu(oc)
+    out32 = case.gpu_decode(cache, q_pos, seq_slot0, seq_len, max_len, flags=flags | tq.OUT_FP32)
+    out16 = case.gpu_decode(cache, q_pos, seq_slot0, seq_len, max_len, flags=flags) if case.io == "f16" else None
+    torch.cuda.synchronize()
+    ref = case.oracle_decode(oc, q_pos, seq_slot0, seq_len, flags=flags)
+    got = _compare(case, out32.cpu().numpy(), None if out16 is None else out16.cpu().numpy(), ref)
+    return got, ref, cache
+
+
+def _oracle_cache(case, L, H):
+    oc = oracle.Cache(L, H, case.slots)
+    case.oracle_quantize(oc)
+    return oc
 
 
 def test_decode_tiny_fp32_workload():
     # 1 layer, 1 head, 256 cached tokens, fp32 I/O, one query at position 256.
     case = Case(20260, 1, 1, 1, 256, io="f32", slots=320, slot0=[0])
-    cache = tq.Cache(1, 1, 320)
-    case.gpu_quantize(cache)
-    _decode_check(case, cache, [256], [0], [256], 256)
+    _decode_check(case, _oracle_cache(case, 1, 1), [256], [0], [256], 256)
 
 
 @pytest.mark.parametrize("flags", [tq.V_ROTATE, 0, tq.V_ROTATE | tq.V_QJL, tq.QJL_PAPER,
@@ -185,18 +200,14 @@ def test_decode_tiny_fp32_workload():
                                    tq.ROPE_HALF | tq.V_ROTATE])
 def test_decode_flags(flags):
     case = Case(21, 2, 4, 2, 300, io="f16", flags=flags, slots=2 * 384, slot0=[0, 384])
-    cache = tq.Cache(2, 4, case.slots)
-    case.gpu_quantize(cache)
-    _decode_check(case, cache, [300, 310], [0, 384], [300, 257], 320)
+    _decode_check(case, _oracle_cache(case, 2, 4), [300, 310], [0, 384], [300, 257], 320)
 
 
 @pytest.mark.parametrize("lens", [[1], [63], [64], [65], [0], [1024], [1025]])
 def test_decode_lengths(lens):
     n = max(lens)
     case = Case(22, 1, 3, len(lens), max(n, 1), io="f16", slots=1088)
-    cache = tq.Cache(1, 3, 1088)
-    case.gpu_quantize(cache)
-    got, ref = _decode_check(case, cache, [n], [0], lens, max(n, 1))
+    got, ref, _ = _decode_check(case, _oracle_cache(case, 1, 3), [n], [0], lens, max(n, 1))
     if lens[0] == 0:
         assert np.all(got == 0)
 
@@ -208,14 +219,14 @@ def test_decode_ragged_batch_and_split_k():
     lens = g.integers(1, 1100, B).astype(np.int32)
     offs, slots = synth.tile_aligned_offsets(lens)
     case = Case(23, 1, 5, B, int(lens.max()), io="f16", slots=slots, slot0=offs)
-    cache = tq.Cache(1, 5, slots)
-    # quantize each sequence's own length
+    oc = oracle.Cache(1, 5, slots)
+    # each sequence's own tokens into its own range
     for b in range(B):
-        sl = slice(0, int(lens[b]))
-        case.gpu_quantize(cache, k=case.t("k")[:, b:b + 1, sl].contiguous(),
-                          v=case.t("v")[:, b:b + 1, sl].contiguous(), pos0=[0], slot0=[int(offs[b])])
+        n = int(lens[b])
+        case.oracle_quantize(oc, k=case.k[:, b:b + 1, :n], v=case.v[:, b:b + 1, :n], pos0=[0],
+                             slot0=[int(offs[b])])
     qpos = lens.copy()
-    _decode_check(case, cache, qpos, offs, lens, int(lens.max()))
+    _, _, cache = _decode_check(case, oc, qpos, offs, lens, int(lens.max()))
     # a larger max_len bound (more splits) gives the same answer within rounding
     out_a = case.gpu_decode(cache, qpos, offs, lens, int(lens.max()), flags=case.flags | tq.OUT_FP32)
     out_b = case.gpu_decode(cache, qpos, offs, lens, int(slots), flags=case.flags | tq.OUT_FP32)
@@ -246,16 +257,25 @@ def test_decode_is_deterministic():
 
 def test_decode_steps_append_then_attend():
     # one layer of 20 heads: prefill 1024 tokens, then 8 steps of
-    # (quantize the new token at position len, attend over len + 1 tokens)
+    # (quantize the new token at position len, attend over len + 1 tokens),
+    # end to end on both sides: the GPU quantizes and attends on its cache,
+    # the oracle on its own
     L, H, T, steps = 1, 20, 1024, 8
     case = Case(20261, L, H, 1, T + steps, io="f16", slots=1088, slot0=[0])
     cache = tq.Cache(L, H, 1088)
+    oc = oracle.Cache(L, H, 1088)
     case.gpu_quantize(cache, k=case.t("k")[:, :, :T].contiguous(), v=case.t("v")[:, :, :T].contiguous())
+    case.oracle_quantize(oc, k=case.k[:, :, :T], v=case.v[:, :, :T])
     for s in range(steps):
         n = T + s
         case.gpu_quantize(cache, k=case.t("k")[:, :, n:n + 1].contiguous(),
                           v=case.t("v")[:, :, n:n + 1].contiguous(), pos0=[n], slot0=[n])
-        _decode_check(case, cache, [n], [0], [n + 1], 1088)
+        case.oracle_quantize(oc, k=case.k[:, :, n:n + 1], v=case.v[:, :, n:n + 1], pos0=[n], slot0=[n])
+        out32 = case.gpu_decode(cache, [n], [0], [n + 1], 1088, flags=case.flags | tq.OUT_FP32)
+        out16 = case.gpu_decode(cache, [n], [0], [n + 1], 1088)
+        torch.cuda.synchronize()
+        ref = case.oracle_decode(oc, [n], [0], [n + 1])
+        _compare(case, out32.cpu().numpy(), out16.cpu().numpy(), ref)
 
 
 # ---------------------------------------------------------------- calibration

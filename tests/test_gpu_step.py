@@ -2,14 +2,15 @@
 fuses, tq_quantize_pack with T = 1 followed by tq_decode_attend: the cache
 bytes and the output must be identical, bit for bit, since the step runs the
 same quantizer and attention arithmetic. Each step is also checked against
-the oracle. Ragged batches, every flag combination, empty caches, split
+the oracle, which quantizes the same tokens into a cache of its own. Ragged batches, every flag combination, empty caches, split
 sequences and invalid sequences are covered."""
 import numpy as np
 import pytest
 import torch
 
 import paper_2603_26110_amd as tq
-from gpu_cases import Case, to_oracle
+from gpu_cases import Case
+from oracle import oracle
 from paper_2603_26110_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -112,11 +113,15 @@ def test_step_equals_append_then_attend_split_sequence():
 
 
 def test_steps_match_oracle():
-    # one layer of 20 heads: prefill 1024 tokens, then 6 decode steps
+    # one layer of 20 heads: prefill 1024 tokens, then 6 decode steps, end to
+    # end on both sides: the GPU steps on its cache, the oracle quantizes the
+    # same tokens into its own cache and attends there
     L, H, T, steps = 1, 20, 1024, 6
     case = Case(20262, L, H, 1, T + steps, io="f16", slots=1088, slot0=[0])
     cache = tq.Cache(L, H, 1088)
     _prefill(case, cache, [T], [0])
+    oc = oracle.Cache(L, H, 1088)
+    case.oracle_quantize(oc, k=case.k[:, :, :T], v=case.v[:, :, :T])
     flags = case.flags | tq.OUT_FP32
     for s in range(steps):
         n = T + s
@@ -124,7 +129,8 @@ def test_steps_match_oracle():
         v = case.t("v")[:, :, n].contiguous()
         out = _step(case, cache, k, v, [n], [0], [n], 1088, flags)
         torch.cuda.synchronize()
-        ref = case.oracle_decode(to_oracle(cache), [n], [0], [n + 1])
+        case.oracle_quantize(oc, k=case.k[:, :, n:n + 1], v=case.v[:, :, n:n + 1], pos0=[n], slot0=[n])
+        ref = case.oracle_decode(oc, [n], [0], [n + 1])
         err = np.abs(out.cpu().numpy().astype(np.float64) - ref)
         assert np.max(err) <= TOL, (s, np.max(err))
     # the appended codes are those of the prefill quantizer for the same tokens
