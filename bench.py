@@ -235,7 +235,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(tq, params, reps[0], S, lut, pi, q, L, H, slots, n_ctx, args.cpu_seconds)
+        cpu = cpu_baseline(k_all, v_all, S, lut, pi, q, L, H, slots, n_ctx, args.cpu_seconds)
 
     line = {
         "metric": "fused 3-bit decode attention: KV GB/s (% HBM peak) and decode steps/s",
@@ -336,40 +336,47 @@ def measured_traffic(workload):
     return int(rec["traffic_bytes_per_step"]), os.path.relpath(path, ROOT)
 
 
-def cpu_baseline(tq, params, rep, S, lut, pi, q, L, H, slots, n_ctx, seconds):
-    """The CPU oracle decode (fp64, OpenMP over units) on the same packed cache
-    bytes, timed on the host. Sample: whole decode steps of this workload,
-    repeated until ~`seconds` of CPU time; value in KV GB/s like the GPU line."""
-    import torch
+def cpu_baseline(k_all, v_all, S, lut, pi, q, L, H, slots, n_ctx, seconds):
+    """The CPU oracle on the same workload, timed on the host: it quantizes
+    the cached tokens into a cache of its own (untimed, like the GPU's
+    prefill), then each timed run is one oracle step: append the new token of
+    every (layer, head) and decode (fp64, OpenMP over units). If one run over
+    all units would exceed `seconds`, the decode covers a leading subset of
+    units; runs repeat until ~`seconds`. Value in KV GB/s like the GPU line."""
     from oracle import oracle
+    T = n_ctx - 1
     oc = oracle.Cache(L, H, slots)
-    oc.k[:] = rep["cache"].k_codes.cpu().numpy()
-    oc.v[:] = rep["cache"].v_codes.cpu().numpy()
-    oc.s[:] = rep["cache"].scalars.cpu().numpy().view(np.uint16)
     cs = oracle.rope_table(slots + 64)
+    oracle.quantize_pack(oc, 1, cs, k_all[:, :, :T], v_all[:, :, :T], [0], [0], pi, lut, lut, S)
+    k_new, v_new = k_all[:, :, T:T + 1], v_all[:, :, T:T + 1]
     qf = np.asarray(q, np.float32)
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+    def run(units):
+        oracle.quantize_pack(oc, 1, cs, k_new, v_new, [T], [T], pi, lut, lut, S)
+        oracle.decode(oc, 1, cs, qf, [T], [0], [n_ctx], pi, lut, lut, S, units=units)
+
     runs, t_total = 0, 0.0
     units_per_run = L * H
     # one step over all units may be long; time a unit subset if so
     sample = None
+    n_probe = min(32, L * H)
     t0 = time.perf_counter()
-    oracle.decode(oc, 1, cs, qf, [n_ctx - 1], [0], [n_ctx], pi, lut, lut, S, units=np.arange(min(32, L * H)))
+    run(np.arange(n_probe))
     probe = time.perf_counter() - t0
-    est_full = probe * (L * H) / min(32, L * H)
-    if est_full > seconds:
-        nu = max(1, int(seconds / probe * min(32, L * H)))
+    if probe * (L * H) / n_probe > seconds:
+        nu = max(1, int(seconds / probe * n_probe))
         sample = np.arange(min(nu, L * H))
         units_per_run = len(sample)
     while t_total < seconds:
         t0 = time.perf_counter()
-        oracle.decode(oc, 1, cs, qf, [n_ctx - 1], [0], [n_ctx], pi, lut, lut, S, units=sample)
+        run(sample)
         t_total += time.perf_counter() - t0
         runs += 1
     kv = units_per_run * n_ctx * 72 * runs
     return {"value": round(kv / t_total / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": f"{runs} decode pass(es) over {units_per_run} of {L * H} (layer, head) units x "
-                      f"{n_ctx} tokens, fp64, {t_total:.1f} s"}
+            "sample": f"{runs} oracle step(s): append of the new token to all {L * H} (layer, head) units, "
+                      f"then fp64 decode of {units_per_run} of them over {n_ctx} tokens, {t_total:.1f} s"}
 
 
 if __name__ == "__main__":
