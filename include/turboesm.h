@@ -186,12 +186,11 @@ TQ_API tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache
  *           A sequence whose range or query position is invalid gets NaN output.
  *   max_len host bound on every seq_len (sizes the split-K grid), >= 0.
  *   out     device [nlayers][B][H][64]: io_dtype, or fp32 with TQ_OUT_FP32.
- *   workspace device, >= tq_decode_workspace_bytes(...) bytes, 16-byte aligned.
- *           It holds the rotated query q^ and u of every unit (written by a
- *           first kernel, read by the attention kernel) and, when long
- *           sequences are split across blocks, the split partials and one
- *           counter per unit. It must be zero-filled before its first use;
- *           every call leaves the counters at zero again.
+ *   workspace device, >= tq_decode_workspace_bytes(...) bytes, 16-byte aligned
+ *           (NULL when that is 0). When long sequences are split across
+ *           blocks it holds the split partials and one counter per unit; it
+ *           must be zero-filled before its first use, and every call leaves
+ *           the counters at zero again.
  *           Calls that share a workspace must be ordered on one stream.
  */
 TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache,
@@ -207,9 +206,10 @@ TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache
  * layer, sequence b and head, first append the new token exactly as
  * tq_quantize_pack with T = 1, pos0 = pos and slot0 = seq_slot0 + seq_len
  * would (same codes), then attend as tq_decode_attend with q_pos = pos and
- * seq_len[b] + 1 cached tokens (same output). One kernel rotates the query
- * and quantizes the new key and value of each (layer, sequence, head) with a
- * single read of its Pi; the attention kernel follows.
+ * seq_len[b] + 1 cached tokens (same output). It is one kernel: the block of
+ * each (layer, sequence, head) quantizes the new key and value with the Pi it
+ * reads for the query, then attends, taking the new token's codes from where
+ * it wrote them.
  *
  *   q, k, v device [nlayers][B][H][64] io_dtype, before RoPE; 16-byte aligned.
  *           k and v are the new token's key and value.
@@ -235,8 +235,9 @@ TQ_API tq_status tq_decode_step(const tq_params* params, const tq_cache* cache,
                          void* out, void* workspace, size_t workspace_bytes,
                          void* stream);
 
-/* Workspace bytes tq_decode_attend and tq_decode_step need for these sizes
- * (0 only for empty or invalid sizes). */
+/* Workspace bytes tq_decode_attend and tq_decode_step need for these sizes:
+ * 0 unless sequences are split across blocks (few units, long max_len), and
+ * 0 for empty or invalid sizes. */
 TQ_API size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B,
                                  int32_t nlayers, int32_t max_len);
 

@@ -125,7 +125,7 @@ size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B, int32_t nla
   const int64_t units = (int64_t)nlayers * B * params->num_heads;
   int waves, nsplit, split_tiles;
   tq::decode_plan((int)std::min<int64_t>(units, 1 << 30), max_len, &waves, &nsplit, &split_tiles);
-  size_t bytes = align256((size_t)units * 2 * 64 * sizeof(float));          // q^ and u per unit
+  size_t bytes = 0;
   if (nsplit > 1) {
     bytes += align256((size_t)units * nsplit * tq::kPartialFloats * sizeof(float));
     bytes += (size_t)units * sizeof(uint32_t);
@@ -189,8 +189,6 @@ tq_status decode_common(const tq_params* params, const tq_cache* cache, const vo
   a.nsplit = nsplit; a.split_tiles = split_tiles;
   a.k_new = k; a.v_new = v; a.append = step ? 1 : 0; a.len_add = step ? 1 : 0;
   char* ws = (char*)workspace;
-  a.qu = (float*)ws;
-  ws += align256((size_t)units * 2 * 64 * sizeof(float));
   if (nsplit > 1) {
     a.partials = (float*)ws;
     ws += align256((size_t)units * nsplit * tq::kPartialFloats * sizeof(float));

@@ -1,25 +1,22 @@
 // Fused decode attention over the packed 3-bit cache (TurboESM Sec. 3.1
-// decode steps 1-4; Algorithm 1 of Sec. 4.3), as two kernels.
+// decode steps 1-4; Algorithm 1 of Sec. 4.3), one kernel per call.
 //
-// decode_prep_kernel (one block per (sequence, layer, head) unit)
-//   q^ = Pi RoPE(q) and u = S q^ (u = q^ for the per-element residual form),
-//   written to the workspace. Rotating the query once replaces the per-key
-//   inverse rotation of Algorithm 1 (identical by Eq. 4). Each row of Pi is
-//   shared by 4 contiguous lanes; a lane applies RoPE to its 16-element slice
-//   of q in registers and the lanes of a row combine their partial sums with
-//   DPP. For a decode step (APPEND) the same block first quantizes the new
-//   key and value into the cache (quantize-then-attend), reusing its read of
-//   Pi: the wave-per-vector quantizer of the append kernel, on Pi and S
-//   staged in LDS.
-//
-// decode_kernel (one block of WAVES waves per unit, or per split of its tiles)
-//   The cache read is bandwidth-bound and, with every block streaming at
-//   once, a load issued behind the stream waits for it. So the block's own
-//   small inputs (q^ and u, the two tables, the sequence's bounds) come
-//   through scalar loads, all issued together before anything else; the
-//   block's first tiles are requested after its tables are built, and Pi for
-//   the epilogue goes straight into LDS after the last prologue barrier.
-//   prologue  two LDS tables per unit: a pair table
+// decode_kernel (one block of WAVES waves per (sequence, layer, head) unit, or
+// per split of its tiles)
+//   loads     Pi and S are copied straight from global memory into LDS
+//             (16-byte direct copies into the Swz16 layout), before anything
+//             else; the sequence's bounds and the two tables of levels come
+//             through scalar loads. The block's first tiles are requested
+//             once Pi has arrived, so that Pi does not queue behind them.
+//   prologue  wave 0: q^ = Pi RoPE(q) and u = S q^ (u = q^ for the
+//             per-element residual form). Rotating the query once replaces
+//             the per-key inverse rotation of Algorithm 1 (identical by
+//             Eq. 4). For a decode step (quantize-then-attend) waves 1 and 2
+//             meanwhile quantize the new key and value into the cache with the
+//             wave-per-vector quantizer of the append kernel, on the same
+//             staged Pi and S; the block whose tiles include the new token
+//             substitutes its codes in the registers of that tile instead of
+//             reading them back. Then two LDS tables per unit: a pair table
 //               T_A[p][a + 8 b] = q^_{2p} c_K[a] + q^_{2p+1} c_K[b]
 //             (one read scores two dimensions' table terms) and a sign table
 //               T_B[w][s] = sum_j u_{8w+j} (2 s_j - 1)
@@ -32,16 +29,16 @@
 //             raised only when a tile max exceeds it by more than 2^8.
 //             Values are accumulated one lane per dimension from the
 //             dimension-major V tile; a tile's token weights reach the lanes
-//             through DPP row broadcasts.
+//             through DPP row broadcasts. Two tiles per wave are in flight.
 //   merge     waves merge through LDS; splits of a unit merge through a
 //             workspace of (m, l, o) partials written and read with
 //             agent-scope atomics: the last split to finish (atomic counter)
 //             combines them by log-sum-exp.
-//   epilogue  o = Pi^T (o^ / l) (one inverse rotation), plus the V residual
-//             estimate alpha S^T s or ebar_V s when V carries sign bits.
+//   epilogue  o = Pi^T (o^ / l) (one inverse rotation, Pi still in LDS), plus
+//             the V residual estimate alpha S^T s or ebar_V s when V carries
+//             sign bits.
 // Work items are dealt so that all splits of a unit land on one XCD (blocks
-// go to the 8 XCDs round-robin), and each unit's prep block runs on the XCD
-// of its decode blocks.
+// go to the 8 XCDs round-robin), where Pi stays in that XCD's L2.
 #include <stdlib.h>
 
 #include "tq_append.hpp"
@@ -265,49 +262,6 @@ __device__ __forceinline__ void value_sign_word(const TileWeights& tg, uint32_t 
   fma_row_bcast<K0 + 7>(acc, rj, sgn[7]);
 }
 
-// N consecutive elements of an fp16 or fp32 vector, in two steps so that all
-// prologue loads are in flight before the first wait: load_raw issues the
-// 16-byte loads (element e0 is a multiple of 8, so they are aligned) and
-// to_float converts after the remaining loads have been issued.
-template <int N>
-struct RawSlice {
-  uint4 w[N / 4];
-};
-
-template <int N>
-__device__ __forceinline__ void load_raw(const void* p, int64_t e0, bool f16, RawSlice<N>& r) {
-  if (f16) {
-    const uint4* q = reinterpret_cast<const uint4*>(reinterpret_cast<const __half*>(p) + e0);
-#pragma unroll
-    for (int j = 0; j < N / 8; ++j) r.w[j] = q[j];
-  } else {
-    const uint4* q = reinterpret_cast<const uint4*>(reinterpret_cast<const float*>(p) + e0);
-#pragma unroll
-    for (int j = 0; j < N / 4; ++j) r.w[j] = q[j];
-  }
-}
-
-template <int N>
-__device__ __forceinline__ void to_float(const RawSlice<N>& r, bool f16, float (&x)[N]) {
-  if (f16) {
-#pragma unroll
-    for (int j = 0; j < N / 8; ++j) {
-      const uint32_t ws[4] = {r.w[j].x, r.w[j].y, r.w[j].z, r.w[j].w};
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        x[8 * j + 2 * k] = half_bits_to_float(ws[k]);
-        x[8 * j + 2 * k + 1] = half_bits_to_float(ws[k] >> 16);
-      }
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < N / 4; ++j) {
-      x[4 * j] = __uint_as_float(r.w[j].x); x[4 * j + 1] = __uint_as_float(r.w[j].y);
-      x[4 * j + 2] = __uint_as_float(r.w[j].z); x[4 * j + 3] = __uint_as_float(r.w[j].w);
-    }
-  }
-}
-
 
 // Pointers into the constant address space (4): same 64-bit addresses, but a
 // load through them with a wave-uniform address is always a scalar load.
@@ -345,346 +299,263 @@ struct Lut8 {
   }
 };
 
-// ------------------------------------------------------------------ prep kernel
-// Unit of prep block `bid`: the XCD of a unit's decode blocks is
-// (unit * nsplit) / per_xcd; prep blocks are dealt to the same XCD.
-// With APPEND (decode step) the block first stages Pi and S in LDS and,
-// after q^ and u are written, waves 0 and 1 quantize and append the new key
-// and value of the unit with the same functions as the append kernel.
-// F16: q, k, v are fp16 (else fp32). HALF: RoPE pairs (m, m + 32).
-template <bool APPEND, bool F16, bool HALF>
-__global__ __launch_bounds__(256) void decode_prep_kernel(DecodeArgs a, int units, int per_xcd) {
-  constexpr int COLS = 16;                 // 4 lanes per row of Pi / S
-  __shared__ float s_qh[kDim];
-  __shared__ VectorSmem sm;                // APPEND only (the compiler drops it otherwise)
-  // Every argument field the block reads, in one batch met by one wait (the
-  // asm uses them all), so that no data load waits behind a constant load.
-  const int nsplit = a.nsplit, H = a.H, B = a.B, layer0 = a.layer0, rope_positions = a.rope_positions;
-  const int len_add = a.len_add, max_len = a.max_len;
-  const int64_t slots = a.slots;
-  const uint32_t flags = a.flags;
-  const float *pi_base = a.pi, *s_base = a.qjl_s, *cs_base = a.rope_cs;
-  const void* q_base = a.q;
-  const int32_t *qpos_p = a.q_pos, *len_p = a.seq_len;
-  const int64_t* s0_p = a.seq_slot0;
-  asm volatile("" ::"s"(nsplit), "s"(H), "s"(B), "s"(layer0), "s"(rope_positions), "s"(len_add),
-               "s"(max_len), "s"(slots), "s"(flags), "s"(pi_base), "s"(s_base), "s"(cs_base),
-               "s"(q_base), "s"(qpos_p), "s"(len_p), "s"(s0_p));
-  // (32-bit: the host keeps units * nsplit, and so 8 * per_xcd, below 2^31)
-  const unsigned x = blockIdx.x % kXcds, j = blockIdx.x / kXcds;
-  const unsigned ns = (unsigned)nsplit, px = (unsigned)per_xcd;
-  const unsigned first = (x * px + ns - 1) / ns;
-  const unsigned next = ((x + 1) * px + ns - 1) / ns;
-  const unsigned unit_u = first + j;
-  if (unit_u >= next || unit_u >= (unsigned)units) return;
-  const int unit = (int)unit_u;
-  const int h = unit % H;
-  const int b = (unit / H) % B;
-  const int l = layer0 + unit / (H * B);
-  const int lh = l * H + h;
-  const int t = threadIdx.x;
-  const int row = t >> 2, c0 = (t & 3) * COLS;
-  const int wave = __builtin_amdgcn_readfirstlane(t >> 6), i = t & 63;
-  const bool paper = (flags & kQjlPaper) != 0;
 
-  // Loads first, none behind a check: Pi and S row slices, q, and for a step
-  // the new key (wave 0) or value (wave 1) with its table levels. Then the
-  // sequence's position, length and first slot (scalar loads, one wait), and
-  // the RoPE row of the position (clamped into the table, so it is requested
-  // as soon as the position arrives, before the checks).
-  const float4* pi_row = reinterpret_cast<const float4*>(pi_base + (int64_t)lh * kDim * kDim + row * kDim + c0);
-  const float4* s_row = reinterpret_cast<const float4*>(s_base + row * kDim + c0);
-  float4 pr[COLS / 4], sr[COLS / 4];
-#pragma unroll
-  for (int k = 0; k < COLS / 4; ++k) pr[k] = pi_row[k];
-#pragma unroll
-  for (int k = 0; k < COLS / 4; ++k) sr[k] = s_row[k];
-  RawSlice<COLS> qraw, praw;
-  load_raw<COLS>(q_base, (int64_t)unit * kDim + c0, F16, qraw);
-  if (HALF) load_raw<COLS>(q_base, (int64_t)unit * kDim + (c0 ^ 32), F16, praw);
-  float xa = 0.0f;
-  Levels La{};
-  if (APPEND) {
-    xa = load_in(wave == 1 ? a.v_new : a.k_new, (int64_t)unit * kDim + i, F16);
-    La = load_levels((wave == 1 ? a.lut_v : a.lut_k) + lh * 8);
-  }
-  const int qp = to_const(qpos_p)[b];
-  const int len = to_const(len_p)[b];
-  const int64_t s0 = to_const(s0_p)[b];
-  asm volatile("" ::"s"(qp), "s"(len), "s"(s0));
-  const int qpc = min(max(qp, 0), rope_positions - 1);
-  const float4* cs_row = reinterpret_cast<const float4*>(cs_base + (int64_t)qpc * 2 * kPairs);
-  float4 csv[COLS / 2];
-  if (HALF) {
-#pragma unroll
-    for (int k = 0; k < COLS / 2; ++k) csv[k] = cs_row[(c0 & 31) / 2 + k];   // pairs (c0 & 31) ..
-  } else {
-#pragma unroll
-    for (int k = 0; k < COLS / 4; ++k) csv[k] = cs_row[c0 / 4 + k];          // pairs c0/2 ..
-  }
-  float2 csk = make_float2(1.0f, 0.0f);
-  if (APPEND)
-    csk = reinterpret_cast<const float2*>(cs_base + (int64_t)qpc * 2 * kPairs)[HALF ? (i & 31) : (i >> 1)];
-
-  const int n = len + len_add;             // tokens attended
-  if (qp < 0 || qp >= rope_positions || n <= 0) return;   // the decode kernel writes 0 or NaN
-  // the new token goes to slot s0 + len exactly when the decode kernel will
-  // accept the sequence (it checks the same bounds for n = len + 1)
-  const bool do_append = APPEND && len >= 0 && n <= max_len && s0 >= 0 && (s0 & 63) == 0 &&
-                         s0 + n <= slots;
-  if (do_append) {
-    // Pi and S for the wave-per-vector quantizer: this thread holds columns
-    // c0 .. c0 + 15 of row `row`
-#pragma unroll
-    for (int k = 0; k < COLS / 4; ++k) {
-      stage_row4(sm.pi, row, c0 + 4 * k, pr[k]);
-      stage_row4(sm.s, row, c0 + 4 * k, sr[k]);
-    }
-  }
-
-  // q' = RoPE(q) in registers (x'_a = x_a c - x_b s, x'_b = x_a s + x_b c)
-  float qx[COLS], qy[COLS], qr[COLS];
-  to_float<COLS>(qraw, F16, qx);
-  if (HALF) {
-    to_float<COLS>(praw, F16, qy);
-#pragma unroll
-    for (int k = 0; k < COLS; ++k) {
-      const float4 v = csv[k / 2];
-      const float c = (k & 1) ? v.z : v.x, sn = (k & 1) ? v.w : v.y;
-      qr[k] = (c0 + k) < 32 ? (qx[k] * c - qy[k] * sn) : (qy[k] * sn + qx[k] * c);
-    }
-  } else {
-#pragma unroll
-    for (int k = 0; k < COLS; k += 2) {
-      const float4 v = csv[k / 4];
-      const float c = (k & 2) ? v.z : v.x, sn = (k & 2) ? v.w : v.y;
-      qr[k] = qx[k] * c - qx[k + 1] * sn;
-      qr[k + 1] = qx[k] * sn + qx[k + 1] * c;
-    }
-  }
-  float acc = 0.0f;
-#pragma unroll
-  for (int k = 0; k < COLS / 4; ++k) {
-    acc = fmaf(pr[k].x, qr[4 * k + 0], acc);
-    acc = fmaf(pr[k].y, qr[4 * k + 1], acc);
-    acc = fmaf(pr[k].z, qr[4 * k + 2], acc);
-    acc = fmaf(pr[k].w, qr[4 * k + 3], acc);
-  }
-  acc += dpp<0xB1>(acc);               // quad_perm [1,0,3,2]
-  acc += dpp<0x4E>(acc);               // quad_perm [2,3,0,1]: every lane of the row has q^_row
-  const float qh_row = acc;
-  float* qu = a.qu + (int64_t)unit * 2 * kDim;
-  if ((t & 3) == 0) { s_qh[row] = qh_row; qu[row] = qh_row; }
-  float u_row = qh_row;
-  if (!paper) {
-    lds_barrier();
-    float up = 0.0f;
-#pragma unroll
-    for (int k = 0; k < COLS / 4; ++k) {
-      const float4 v = *reinterpret_cast<const float4*>(s_qh + c0 + 4 * k);
-      up = fmaf(sr[k].x, v.x, up);
-      up = fmaf(sr[k].y, v.y, up);
-      up = fmaf(sr[k].z, v.z, up);
-      up = fmaf(sr[k].w, v.w, up);
-    }
-    up += dpp<0xB1>(up);
-    up += dpp<0x4E>(up);
-    u_row = up;
-  }
-  if ((t & 3) == 1) qu[kDim + row] = u_row;
-
-  if (do_append) {
-    lds_barrier();                     // Pi and S staged
-    if (wave < 2) {
-      const bool is_v = wave == 1;
-      const int ksign = paper ? 2 : 1;
-      const int sign_mode = is_v ? ((a.flags & kVQjl) ? ksign : 0) : ksign;
-      const bool rotate = !is_v || (a.flags & kVRotate);
-      const float xr = is_v ? xa : rope_wave(xa, csk, HALF, i);
-      append_wave(xr, is_v, rotate, La, sm, sign_mode, s0 + len, lh, const_cast<uint8_t*>(a.k_codes),
-                  const_cast<uint8_t*>(a.v_codes), const_cast<uint16_t*>(a.scalars), a.slots, i, wave);
-    }
+// The appended token's codes as the append wrote them into LDS
+// (s_new = [n_k | g_k, n_v | g_v], key words 0..7, value nibbles of
+// dimensions 0..63) replace row `row` of a tile loaded before the append:
+// the key words and scalars of lane `row`, and in every lane (a dimension)
+// the row's nibble of the value word of its 8-token group.
+__device__ __forceinline__ void patch_new_token(TileRegs& r, const uint32_t* s_new, int row, int lane) {
+  const bool mine = lane == row;
+  const uint4 k0 = make_uint4(s_new[2], s_new[3], s_new[4], s_new[5]);
+  const uint4 k1 = make_uint4(s_new[6], s_new[7], s_new[8], s_new[9]);
+  const uint32_t sk = s_new[0], sv = s_new[1];
+  r.k0.x = mine ? k0.x : r.k0.x; r.k0.y = mine ? k0.y : r.k0.y;
+  r.k0.z = mine ? k0.z : r.k0.z; r.k0.w = mine ? k0.w : r.k0.w;
+  r.k1.x = mine ? k1.x : r.k1.x; r.k1.y = mine ? k1.y : r.k1.y;
+  r.k1.z = mine ? k1.z : r.k1.z; r.k1.w = mine ? k1.w : r.k1.w;
+  r.sc.x = mine ? sk : r.sc.x;
+  r.sc.y = mine ? sv : r.sc.y;
+  const uint32_t sh = 4u * (uint32_t)(row & 7);
+  const uint32_t nib = s_new[10 + lane] << sh, keep = ~(15u << sh);
+  uint4& v = (row < 32) ? r.v0 : r.v1;   // row is wave-uniform
+  switch ((row & 31) >> 3) {
+    case 0: v.x = (v.x & keep) | nib; break;
+    case 1: v.y = (v.y & keep) | nib; break;
+    case 2: v.z = (v.z & keep) | nib; break;
+    default: v.w = (v.w & keep) | nib; break;
   }
 }
-
 
 template <int WAVES, bool VQJL>
 __global__ __launch_bounds__(WAVES * 64)
 __attribute__((amdgpu_waves_per_eu((WAVES == 8 && !VQJL) ? 6 : 1)))
 void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
-  constexpr int TAM = 2048 / (WAVES * 64);   // pair-table entries per thread
-  constexpr int TBM = 512 / (WAVES * 64);    // groups of 4 sign-table entries per thread
-  constexpr int COLS = kDim / WAVES;       // rows of Pi per thread in the epilogue
-  constexpr int DEPTH = (WAVES == 8) ? 1 : 2;
   constexpr int NT = WAVES * 64;
-  constexpr int PIV = 1024 / NT;          // float4 of Pi per thread
-  __shared__ float s_ta[32 * 64];          // pair table of the score's table term
-  __shared__ __attribute__((aligned(16))) float s_tb[8 * 256];   // sign-byte table of the QJL term
-  __shared__ __attribute__((aligned(16))) float s_pi[kDim * kDim];
+  constexpr int TAM = 2048 / NT;           // pair-table entries per thread
+  constexpr int TBM = 512 / NT;            // groups of 4 sign-table entries per thread
+  constexpr int COLS = kDim / WAVES;       // rows of Pi per thread in the epilogue
+  constexpr int DEPTH = 2;                 // tiles in flight per wave
+  constexpr int MCH = 1024 / NT;           // 16-byte chunks of a 64 x 64 matrix per thread
+  constexpr int NB = 4;                    // read batch of the prologue's row products
+  __shared__ __attribute__((aligned(16))) float s_pi[kDim * kDim];   // Pi (Swz16)
+  // S (Swz16) in the prologue; after the main loop the merge's scratch
+  __shared__ __attribute__((aligned(16))) float s_ws[kDim * kDim];
+  __shared__ __attribute__((aligned(16))) float s_ta[32 * 64];        // pair table of the score's table term
+  __shared__ __attribute__((aligned(16))) float s_tb[8 * 256];        // sign-byte table of the QJL term
+  // RoPE(q), q^, u, and the staging vectors x, r of the key and value appends
+  __shared__ __attribute__((aligned(16))) float s_vec[7][kDim];
+  __shared__ uint32_t s_new[2 + 8 + kDim];                           // the appended token's codes
   __shared__ float s_vtab[16];
-  __shared__ float s_part[WAVES][kDim];
-  __shared__ float s_wo[WAVES][kDim];
-  __shared__ float s_wsg[VQJL ? WAVES : 1][kDim];
   __shared__ float s_wm[WAVES], s_wl[WAVES];
-  __shared__ float s_oh[kDim], s_sh[kDim];
   __shared__ int s_last;
-  const int bid = blockIdx.x;
-  const int work = (bid % kXcds) * per_xcd + bid / kXcds;
-  if (work >= total_work) return;
+  float* const s_wo = s_ws;                        // [WAVES][64] per-wave o
+  float* const s_wsg = s_ws + WAVES * kDim;        // [WAVES][64] per-wave V sign sums
+  float* const s_part = s_ws + 2 * WAVES * kDim;   // [WAVES][64] epilogue partial products
+  float* const s_oh = s_ws + 3 * WAVES * kDim;     // [64]
+  float* const s_sh = s_oh + kDim;                 // [64]
   // The argument fields the prologue needs, read in one batch and met by one
   // wait (used by the asm), so that no later data load waits on one of them.
-  const int nsplit = a.nsplit, H = a.H, B = a.B, layer0 = a.layer0;
+  const int nsplit = a.nsplit, H = a.H, B = a.B, layer0 = a.layer0, len_add = a.len_add;
+  const int f16_in = a.f16_in, rope_positions = a.rope_positions;
   const uint32_t flags = a.flags;
-  const float *qu_base = a.qu, *lut_k = a.lut_k, *lut_v = a.lut_v, *ebar = a.ebar;
+  const float *lut_k = a.lut_k, *lut_v = a.lut_v, *ebar = a.ebar, *pi_base = a.pi, *s_base = a.qjl_s;
+  const float* rope_cs = a.rope_cs;
+  const void *q_in = a.q, *k_in = a.k_new, *v_in = a.v_new;
   const int32_t* seq_len = a.seq_len;
   const int64_t* seq_slot0 = a.seq_slot0;
   const int32_t* q_pos = a.q_pos;
-  asm volatile("" ::"s"(nsplit), "s"(H), "s"(B), "s"(layer0), "s"(flags), "s"(qu_base), "s"(lut_k),
-               "s"(lut_v), "s"(ebar), "s"(seq_len), "s"(seq_slot0), "s"(q_pos));
+  asm volatile("" ::"s"(total_work), "s"(per_xcd), "s"(nsplit), "s"(H), "s"(B), "s"(layer0), "s"(len_add),
+               "s"(f16_in), "s"(rope_positions), "s"(flags), "s"(lut_k), "s"(lut_v), "s"(ebar), "s"(pi_base),
+               "s"(s_base), "s"(rope_cs), "s"(q_in), "s"(k_in), "s"(v_in), "s"(seq_len), "s"(seq_slot0),
+               "s"(q_pos));
+  const int bid = blockIdx.x;
+  const int work = (bid % kXcds) * per_xcd + bid / kXcds;
+  if (work >= total_work) return;
   const int unit = work / nsplit;
   const int split = work - unit * nsplit;
   const int h = unit % H;
   const int b = (unit / H) % B;
-  const int li = unit / (H * B);
-  const int l = layer0 + li;
+  const int l = layer0 + unit / (H * B);
   const int lh = l * H + h;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-
   const bool paper = (flags & kQjlPaper) != 0;
+  const bool use_s = !paper;               // S enters u = S q^ and the keys' sign bits
 
-  // ------------------------------------------------------- prologue loads
-  // Everything the prologue reads is the same for a whole wave and is fetched
-  // with scalar loads, issued before anything else and before the first store
-  // of the kernel (so the compiler may take the scalar path): the scalar cache
-  // does not queue behind the tile loads that blocks already running on this
-  // compute unit have in its vector memory pipeline, which can hold a late
-  // block's first vector load for several microseconds.
-  // Table entries built by this thread (NT threads):
-  //   ta (2048 entries): e = t + NT m, pair P = e / 64 = wave + NT/64 m, index f = e % 64 = lane
-  //   tb (2048 entries in groups of 4): group e = t + NT m of word w = e / 64,
-  //      sign bytes 4 (e % 64) .. 4 (e % 64) + 3
-  // Read through the constant address space: loads from it with a wave-uniform
-  // address always take the scalar path. (Nothing here changes during a launch:
-  // q^ and u come from the preceding prep kernel.)
-  const cfloat* p_qu = to_const(qu_base);
-  const cfloat* p_lk = to_const(lut_k);
-  const cfloat* p_lv = to_const(lut_v);
-  const cfloat* p_eb = to_const(ebar);
-  const cint32* p_len = to_const(seq_len);
-  const cint64* p_s0 = to_const(seq_slot0);
-  const cint32* p_qp = to_const(q_pos);
-  const cfloat* qu = p_qu + (int64_t)unit * 2 * kDim;
-  const cfloat* lk = p_lk + lh * 8;
-  const cfloat* lv = p_lv + lh * 8;
-  // Loaded as 64-bit pairs: one asm operand each (an asm takes at most 30).
-  uint64_t qw[TAM], uw[TBM][4], kw[4], vw[4];
+  // ---------------------------------------------------------- Pi, S -> LDS
+  // Each wave instruction fills 1 KB of LDS; a lane fetches the global chunk
+  // that belongs at its position.
+  {
+    typedef __attribute__((address_space(3))) void* lds_ptr;
+    const float* pig = pi_base + (int64_t)lh * kDim * kDim;
 #pragma unroll
-  for (int m = 0; m < TAM; ++m) qw[m] = load_pair(qu + 2 * (wave + (NT / 64) * m));
+    for (int j = 0; j < MCH; ++j) {
+      const int c0 = (wave + WAVES * j) * 64;
+      __builtin_amdgcn_global_load_lds(pig + Swz16::source(c0 + lane) * 4, (lds_ptr)(s_pi + c0 * 4), 16, 0, 0);
+    }
+    if (use_s) {
 #pragma unroll
-  for (int m = 0; m < TBM; ++m) {
-    const cfloat* e = qu + kDim + 8 * (wave + (NT / 64) * m);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) uw[m][k] = load_pair(e + 2 * k);
+      for (int j = 0; j < MCH; ++j) {
+        const int c0 = (wave + WAVES * j) * 64;
+        __builtin_amdgcn_global_load_lds(s_base + Swz16::source(c0 + lane) * 4, (lds_ptr)(s_ws + c0 * 4), 16,
+                                         0, 0);
+      }
+    }
   }
+
+  // ------------------------------------------------------ prologue loads
+  // Uniform values through the constant address space (a load from it with a
+  // wave-uniform address always takes the scalar path; the scalar cache does
+  // not queue behind the vector memory pipeline), as 64-bit pairs: one asm
+  // operand each.
+  const cfloat* lk = to_const(lut_k) + lh * 8;
+  const cfloat* lv = to_const(lut_v) + lh * 8;
+  uint64_t kw[4], vw[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     kw[k] = load_pair(lk + 2 * k);
     vw[k] = load_pair(lv + 2 * k);
   }
-  const float ebar_raw = *(paper ? p_eb + lh * 2 : lk);
-  const int n = p_len[b] + a.len_add;
-  const int64_t s0 = p_s0[b];
-  const int qp = p_qp[b];
-  // Every loaded value is used here, before the checks branch: the loads are
-  // independent, so they are all issued and met by one wait (a load is
-  // otherwise free to sink below the branch, one round trip after the other).
-  static_assert(TAM + 4 * TBM + 8 + 4 <= 30, "asm operand limit");
-  if constexpr (TBM == 1) {
-    asm volatile("" ::"s"(qw[0]), "s"(qw[1]), "s"(qw[2]), "s"(qw[3]), "s"(uw[0][0]), "s"(uw[0][1]),
-                 "s"(uw[0][2]), "s"(uw[0][3]), "s"(kw[0]), "s"(kw[1]), "s"(kw[2]), "s"(kw[3]),
-                 "s"(vw[0]), "s"(vw[1]), "s"(vw[2]), "s"(vw[3]), "s"(ebar_raw), "s"(n), "s"(s0),
-                 "s"(qp));
-  } else {
-    asm volatile("" ::"s"(qw[0]), "s"(qw[1]), "s"(qw[2]), "s"(qw[3]), "s"(qw[4]), "s"(qw[5]),
-                 "s"(qw[6]), "s"(qw[7]), "s"(uw[0][0]), "s"(uw[0][1]), "s"(uw[0][2]),
-                 "s"(uw[0][3]), "s"(uw[1][0]), "s"(uw[1][1]), "s"(uw[1][2]), "s"(uw[1][3]),
-                 "s"(kw[0]), "s"(kw[1]), "s"(kw[2]), "s"(kw[3]), "s"(vw[0]), "s"(vw[1]),
-                 "s"(vw[2]), "s"(vw[3]), "s"(ebar_raw), "s"(n), "s"(s0), "s"(qp));
+  const float ebar_raw = *(paper ? to_const(ebar) + lh * 2 : lk);
+  const int len = to_const(seq_len)[b];
+  const int64_t s0 = to_const(seq_slot0)[b];
+  const int qp = to_const(q_pos)[b];
+  // Every scalar value is used here, before anything branches on them: the
+  // loads are independent, so they are all issued and met by one wait.
+  asm volatile("" ::"s"(kw[0]), "s"(kw[1]), "s"(kw[2]), "s"(kw[3]), "s"(vw[0]), "s"(vw[1]), "s"(vw[2]),
+               "s"(vw[3]), "s"(ebar_raw), "s"(len), "s"(s0), "s"(qp));
+  // The vector the wave works on in the prologue, q (wave 0) or a step's
+  // new key (wave 1) or value (wave 2), as raw bits (converted where used,
+  // so that no wait follows the load), and the RoPE (cos, sin) of the lane's
+  // pair at the position, clamped into the table (checked below): both are
+  // requested before the checks.
+  const bool f16 = f16_in != 0;
+  const bool step = a.append != 0;
+  const bool half = (flags & kRopeHalf) != 0;
+  const bool has_vec = wave == 0 || (step && wave <= 2);
+  const void* vsrc = wave == 0 ? q_in : (wave == 1 ? k_in : v_in);
+  uint32_t xraw = 0;
+  if (has_vec) {
+    const int64_t e = (int64_t)unit * kDim + lane;
+    xraw = f16 ? (uint32_t)reinterpret_cast<const unsigned short*>(vsrc)[e] : reinterpret_cast<const uint32_t*>(vsrc)[e];
   }
-  float2 qpair[TAM];
-#pragma unroll
-  for (int m = 0; m < TAM; ++m) qpair[m] = pair_f2(qw[m]);
-  float4 ulo[TBM], uhi[TBM];
-#pragma unroll
-  for (int m = 0; m < TBM; ++m) {
-    const float2 a0 = pair_f2(uw[m][0]), a1 = pair_f2(uw[m][1]);
-    const float2 a2 = pair_f2(uw[m][2]), a3 = pair_f2(uw[m][3]);
-    ulo[m] = make_float4(a0.x, a0.y, a1.x, a1.y);
-    uhi[m] = make_float4(a2.x, a2.y, a3.x, a3.y);
+  float2 cs = make_float2(1.0f, 0.0f);
+  if (wave <= 1) {
+    const int qpc = min(max(qp, 0), rope_positions - 1);
+    cs = reinterpret_cast<const float2*>(rope_cs + (int64_t)qpc * 2 * kPairs)[half ? (lane & 31) : (lane >> 1)];
   }
   const Lut8 ck = Lut8::of(kw), cvl = Lut8::of(vw);
   const float ebar_k = paper ? ebar_raw : 0.0f;
+  const int n = len + len_add;             // tokens attended (the step's new one included)
   const bool valid = (n >= 0) & (n <= a.max_len) & (s0 >= 0) & ((s0 & 63) == 0) &
-                     (s0 + n <= a.slots) & (qp >= 0) & (qp < a.rope_positions);
+                     (s0 + n <= a.slots) & (qp >= 0) & (qp < rope_positions);
   if (!valid || n == 0) {
     if (split == 0 && t < kDim) store_out(a, unit, t, valid ? 0.0f : __int_as_float(0x7FC00000));
+    __builtin_amdgcn_s_waitcnt(0);         // no copy into LDS outlives the block
     return;
   }
   const int ntiles = (n + 63) >> 6;
   const int tile_begin = split * a.split_tiles;
-  if (tile_begin >= ntiles) return;
+  if (tile_begin >= ntiles) {
+    __builtin_amdgcn_s_waitcnt(0);
+    return;
+  }
   const int tile_end = min(ntiles, tile_begin + a.split_tiles);
   const int participants = (ntiles + a.split_tiles - 1) / a.split_tiles;
-  const float ck_lo = ck.pick(lane & 7), ck_hi = ck.pick(lane >> 3);
-  const float cv = cvl.pick(t & 7);
+  // a step's new token (index n - 1) is appended by the block of its tile
+  const int tnew = (n - 1) >> 6, rnew = (n - 1) & 63;
+  const bool app = step && tnew >= tile_begin && tnew < tile_end;
 
   const uint8_t* kreg = a.k_codes + (int64_t)lh * a.slots * 32;
   const uint8_t* vreg = a.v_codes + (int64_t)lh * a.slots * 32;
   const uint2* sreg = reinterpret_cast<const uint2*>(a.scalars + (int64_t)lh * a.slots * 4);
   const int64_t tile0 = s0 >> 6;
-  // --------------------------------------------------------------- prologue
-#pragma unroll
-  for (int m = 0; m < TAM; ++m)
-    s_ta[t + NT * m] = fmaf(qpair[m].y, ck_hi, qpair[m].x * ck_lo);
-#pragma unroll
-  for (int m = 0; m < TBM; ++m) {
-    const int e = t + NT * m, k = e & 63;
-    const float u[8] = {ulo[m].x, ulo[m].y, ulo[m].z, ulo[m].w, uhi[m].x, uhi[m].y, uhi[m].z, uhi[m].w};
-    float base = 0.0f;                 // sign bits 2..7 of the bytes 4k .. 4k+3 are the bits of k
-#pragma unroll
-    for (int j = 2; j < 8; ++j) base += ((k >> (j - 2)) & 1) ? u[j] : -u[j];
-    float4 v;
-    v.x = (base - u[0]) - u[1];
-    v.y = (base + u[0]) - u[1];
-    v.z = (base - u[0]) + u[1];
-    v.w = (base + u[0]) + u[1];
-    reinterpret_cast<float4*>(s_tb)[e] = v;
+
+  // Pi and S have arrived (every wave waits for its own copies, then the
+  // barrier). Only now are the tiles requested: by the waves without
+  // prologue work at once, by the others when it is done (their registers
+  // then hold no tiles during the prologue).
+  __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0)
+  lds_barrier();
+
+  // -------------------------------------------------------------- prologue
+  if (wave == 0) {
+    const float xin = f16 ? half_bits_to_float(xraw) : __uint_as_float(xraw);
+    s_vec[0][lane] = rope_wave(xin, cs, half, lane);
+    wave_sync_lds();
+    const float qh = row_dot<Swz16, NB>(s_pi, s_vec[0], lane);
+    s_vec[1][lane] = qh;
+    float u = qh;
+    if (use_s) {
+      wave_sync_lds();
+      u = row_dot<Swz16, NB>(s_ws, s_vec[1], lane);
+    }
+    s_vec[2][lane] = u;
+  } else if (app && wave <= 2) {
+    const bool is_v = wave == 2;
+    const int ksign = paper ? 2 : 1;
+    const int sign_mode = is_v ? ((flags & kVQjl) ? ksign : 0) : ksign;
+    const bool rotate = !is_v || (flags & kVRotate);
+    const Lut8& c = is_v ? cvl : ck;
+    Levels La;
+    La.c0 = c.c0; La.c1 = c.c1; La.c2 = c.c2; La.c3 = c.c3;
+    La.c4 = c.c4; La.c5 = c.c5; La.c6 = c.c6; La.c7 = c.c7;
+    La.t0 = 0.5f * (La.c0 + La.c1); La.t1 = 0.5f * (La.c1 + La.c2); La.t2 = 0.5f * (La.c2 + La.c3);
+    La.t3 = 0.5f * (La.c3 + La.c4); La.t4 = 0.5f * (La.c4 + La.c5); La.t5 = 0.5f * (La.c5 + La.c6);
+    La.t6 = 0.5f * (La.c6 + La.c7);
+    const float xin = f16 ? half_bits_to_float(xraw) : __uint_as_float(xraw);
+    const float xr = is_v ? xin : rope_wave(xin, cs, half, lane);
+    const Appended ap = append_wave<Swz16, NB>(
+        xr, is_v, rotate, La, s_pi, s_ws, s_vec[is_v ? 5 : 3], s_vec[is_v ? 6 : 4], sign_mode, s0 + (n - 1),
+        lh, const_cast<uint8_t*>(a.k_codes), const_cast<uint8_t*>(a.v_codes),
+        const_cast<uint16_t*>(a.scalars), a.slots, lane);
+    if (!is_v) {
+      if ((lane & 7) == 0) s_new[2 + (lane >> 3)] = ap.code;
+      if (lane == 0) s_new[0] = ap.scal;
+    } else {
+      s_new[10 + lane] = ap.code;
+      if (lane == 0) s_new[1] = ap.scal;
+    }
   }
-  s_vtab[t & 15] = cv;             // every thread: identical values, no branch around the load
-  // The first tiles are requested only now: issuing a vector load can stall
-  // while this compute unit's memory pipeline is full, and the tables above
-  // need nothing from it.
   TileRegs buf[DEPTH];
 #pragma unroll
   for (int d = 0; d < DEPTH; ++d) {
     const int tq = min(tile_begin + wave + d * WAVES, tile_end - 1);   // (a wave without tiles re-reads one)
     load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
   }
-  lds_barrier();
+  lds_barrier();                           // q^, u (and the new token's codes) ready; S no longer read
 
-  // Pi for the epilogue, straight into LDS (1 KB per wave instruction). Issued
-  // after the last barrier before the merge: the compiler makes a barrier wait
-  // for transfers into LDS still in flight.
+  // Table entries built by this thread (NT threads):
+  //   ta (2048 entries): e = t + NT m, pair P = e / 64 = wave + WAVES m, index f = e % 64 = lane
+  //   tb (2048 entries in groups of 4): group e = t + NT m of word w = e / 64,
+  //      sign bytes 4 (e % 64) .. 4 (e % 64) + 3
   {
-    typedef __attribute__((address_space(3))) void* lds_ptr;
-    const float* pig = a.pi + (int64_t)lh * kDim * kDim;
+    const float ck_lo = ck.pick(lane & 7), ck_hi = ck.pick(lane >> 3);
 #pragma unroll
-    for (int j = 0; j < PIV; ++j) {
-      const int chunk = (wave + WAVES * j) * 64;    // first 16-byte chunk of this wave instruction
-      __builtin_amdgcn_global_load_lds(pig + (chunk + lane) * 4, (lds_ptr)(s_pi + chunk * 4), 16, 0, 0);
+    for (int m = 0; m < TAM; ++m) {
+      const float2 qq = reinterpret_cast<const float2*>(s_vec[1])[wave + WAVES * m];
+      s_ta[t + NT * m] = fmaf(qq.y, ck_hi, qq.x * ck_lo);
     }
+#pragma unroll
+    for (int m = 0; m < TBM; ++m) {
+      const int e = t + NT * m, k = e & 63, w = wave + WAVES * m;
+      const float4 ulo = reinterpret_cast<const float4*>(s_vec[2])[2 * w];
+      const float4 uhi = reinterpret_cast<const float4*>(s_vec[2])[2 * w + 1];
+      const float u[8] = {ulo.x, ulo.y, ulo.z, ulo.w, uhi.x, uhi.y, uhi.z, uhi.w};
+      float base = 0.0f;               // sign bits 2..7 of the bytes 4k .. 4k+3 are the bits of k
+#pragma unroll
+      for (int j = 2; j < 8; ++j) base += ((k >> (j - 2)) & 1) ? u[j] : -u[j];
+      float4 v;
+      v.x = (base - u[0]) - u[1];
+      v.y = (base + u[0]) - u[1];
+      v.z = (base - u[0]) + u[1];
+      v.w = (base + u[0]) + u[1];
+      reinterpret_cast<float4*>(s_tb)[e] = v;
+    }
+    s_vtab[t & 15] = cvl.pick(t & 7);   // every thread: identical values
   }
+  lds_barrier();
 
   // -------------------------------------------------------------- main loop
   float m_run = -INFINITY;
@@ -699,6 +570,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     for (int d = 0; d < DEPTH; ++d) {
       const int tt = tb + d * WAVES;
       if (tt >= tile_end) break;
+      if (app && tt == tnew) patch_new_token(buf[d], s_new, rnew, lane);
       const TileRegs& cur = buf[d];
       const int tok = tt * kTile + lane;
       const bool tv = tok < n;
@@ -761,12 +633,11 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   }
 
   // ------------------------------------------------------ merge the waves
-  // (a full barrier: it also waits for this wave's Pi transfer into LDS)
   const float ov = (o0 + o1) + (o2 + o3);
   const float l_wave = wave_sum_uniform(l_lane);
   if (lane == 0) { s_wm[wave] = m_run; s_wl[wave] = l_wave; }
-  s_wo[wave][lane] = ov;
-  if (VQJL) s_wsg[wave][lane] = sg;
+  s_wo[wave * kDim + lane] = ov;
+  if (VQJL) s_wsg[wave * kDim + lane] = sg;
   __syncthreads();
   float M = -INFINITY, L = 0.0f, O = 0.0f, SG = 0.0f;
   if (t < kDim) {
@@ -776,8 +647,8 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     for (int w = 0; w < WAVES; ++w) {
       const float f = __builtin_amdgcn_exp2f(s_wm[w] - M);
       L += s_wl[w] * f;
-      O += s_wo[w][t] * f;
-      if (VQJL) SG += s_wsg[w][t] * f;
+      O += s_wo[w * kDim + t] * f;
+      if (VQJL) SG += s_wsg[w * kDim + t] * f;
     }
   }
 
@@ -868,12 +739,12 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
         const int i = cq * COLS + ii;
         acc = fmaf(a.qjl_s[i * kDim + k], s_sh[i], acc);
       }
-      s_part[cq][k] = acc;
+      s_part[cq * kDim + k] = acc;
       lds_barrier();
       if (t < kDim) {
         float y = 0.0f;
 #pragma unroll
-        for (int w = 0; w < WAVES; ++w) y += s_part[w][t];
+        for (int w = 0; w < WAVES; ++w) y += s_part[w * kDim + t];
         s_oh[t] += kQjlAlpha * y;
       }
     }
@@ -886,14 +757,14 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
     for (int ii = 0; ii < COLS; ++ii) {
       const int i = cq * COLS + ii;
-      acc = fmaf(s_pi[i * kDim + k], s_oh[i], acc);
+      acc = fmaf(s_pi[Swz16::chunk(i, k >> 2) * 4 + (k & 3)], s_oh[i], acc);
     }
-    s_part[cq][k] = acc;
+    s_part[cq * kDim + k] = acc;
     lds_barrier();
     if (t < kDim) {
       float y = 0.0f;
 #pragma unroll
-      for (int w = 0; w < WAVES; ++w) y += s_part[w][t];
+      for (int w = 0; w < WAVES; ++w) y += s_part[w * kDim + t];
       store_out(a, unit, t, y);
     }
   } else {
@@ -933,21 +804,6 @@ hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st) {
   const int64_t per_xcd = (total + kXcds - 1) / kXcds;
   const int64_t blocks = per_xcd * kXcds;
   const bool vq = (a.flags & kVQjl) != 0;
-  // prep blocks: per XCD, the units whose decode blocks run there
-  const int64_t prep_per_xcd = (per_xcd + a.nsplit - 1) / a.nsplit + 1;
-  {
-    const dim3 pg((unsigned)(kXcds * prep_per_xcd)), pb(256);
-    const bool f16 = a.f16_in != 0, half = (a.flags & kRopeHalf) != 0;
-#define TQ_PREP(AP, F, HF) hipLaunchKernelGGL((decode_prep_kernel<AP, F, HF>), pg, pb, 0, st, a, (int)units, (int)per_xcd)
-    if (a.append) {
-      if (f16) { if (half) TQ_PREP(true, true, true); else TQ_PREP(true, true, false); }
-      else     { if (half) TQ_PREP(true, false, true); else TQ_PREP(true, false, false); }
-    } else {
-      if (f16) { if (half) TQ_PREP(false, true, true); else TQ_PREP(false, true, false); }
-      else     { if (half) TQ_PREP(false, false, true); else TQ_PREP(false, false, false); }
-    }
-#undef TQ_PREP
-  }
   if (waves == 8) {
     if (vq)
       hipLaunchKernelGGL((decode_kernel<8, true>), dim3((unsigned)blocks), dim3(512), 0, st, a, (int)total, (int)per_xcd);

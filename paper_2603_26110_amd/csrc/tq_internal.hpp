@@ -51,13 +51,12 @@ struct DecodeArgs {
   const uint16_t* scalars;
   int64_t slots;
   void* out;
-  float* qu;               // [units][2][64]: q^ and u from the prep kernel
   float* partials;         // [units][nsplit][kPartialFloats]
   uint32_t* counters;      // [units]
   int nsplit;              // splits per unit
   int split_tiles;         // 64-token tiles per split
-  // decode step: the prep kernel first appends one token per sequence (its key
-  // and value [nlayers][B][H][64], position q_pos[b], slot seq_slot0[b] +
+  // decode step: the kernel also appends one token per sequence (its key and
+  // value [nlayers][B][H][64], position q_pos[b], slot seq_slot0[b] +
   // seq_len[b]); the attention then covers seq_len[b] + len_add tokens
   const void* k_new;
   const void* v_new;

@@ -259,8 +259,8 @@ __global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, uint
 
   // ---- RoPE (keys), rotation, quantizer, store
   if (!is_v && !rotated) x = rope_wave(x, cs, half, i);
-  append_wave(x, is_v, rotate, L, sm, sign_mode, slot, lh, a.k_codes, a.v_codes, a.scalars, a.slots, i,
-              wave);
+  append_wave<Pitch68>(x, is_v, rotate, L, sm.pi, sm.s, sm.x[wave], sm.r[wave], sign_mode, slot, lh,
+                       a.k_codes, a.v_codes, a.scalars, a.slots, i);
 }
 
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t st) {
