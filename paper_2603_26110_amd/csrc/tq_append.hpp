@@ -58,12 +58,21 @@ __device__ __forceinline__ void wave_sync_lds() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Zero, computed after `x`: an offset that makes the reads of a batch wait
+// for the chain of the one before, so the compiler cannot hoist them (and
+// hold every batch's registers at once).
+__device__ __forceinline__ int after(float x) {
+  int z;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(z) : "v"(x));
+  return z;
+}
+
 // Row i of a 64 x 64 matrix staged in `m` (layout LY) times the vector staged
 // in `v`: fma chain over k ascending, the order of rotate_lane and
 // quantize_lane. The reads are issued in batches of NB chunks of four
-// elements, each batch before its part of the chain (NB = 16: one LDS latency
-// for the whole row; smaller batches hold fewer registers). The batch size
-// changes no arithmetic.
+// elements, each batch after the chain of the one before (NB = 16: one LDS
+// latency for the whole row; smaller batches hold fewer registers). The batch
+// size changes no arithmetic.
 template <class LY, int NB = 16>
 __device__ __forceinline__ float row_dot(const float* m, const float* v, int i) {
   const float4* m4 = reinterpret_cast<const float4*>(m);
@@ -71,11 +80,12 @@ __device__ __forceinline__ float row_dot(const float* m, const float* v, int i) 
   float acc = 0.0f;
 #pragma unroll
   for (int b = 0; b < kDim / 4; b += NB) {
+    const int z = b > 0 ? after(acc) : 0;
     float4 mr[NB], vv[NB];
 #pragma unroll
     for (int k4 = 0; k4 < NB; ++k4) {
-      mr[k4] = m4[LY::chunk(i, b + k4)];
-      vv[k4] = v4[b + k4];
+      mr[k4] = m4[LY::chunk(i, b + k4) + z];
+      vv[k4] = v4[b + k4 + z];
     }
 #pragma unroll
     for (int k4 = 0; k4 < NB; ++k4) {
@@ -96,9 +106,10 @@ __device__ __forceinline__ float sum_squares(const float* v) {
   float acc = 0.0f;
 #pragma unroll
   for (int b = 0; b < kDim / 4; b += NB) {
+    const int z = b > 0 ? after(acc) : 0;
     float4 vv[NB];
 #pragma unroll
-    for (int k4 = 0; k4 < NB; ++k4) vv[k4] = v4[b + k4];
+    for (int k4 = 0; k4 < NB; ++k4) vv[k4] = v4[b + k4 + z];
 #pragma unroll
     for (int k4 = 0; k4 < NB; ++k4) {
       acc = fmaf(vv[k4].x, vv[k4].x, acc);

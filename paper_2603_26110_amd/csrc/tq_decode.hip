@@ -6,22 +6,25 @@
 //   loads     Pi and S are copied straight from global memory into LDS
 //             (16-byte direct copies into the Swz16 layout), before anything
 //             else; the sequence's bounds and the two tables of levels come
-//             through scalar loads. The block's first tiles are requested
-//             once Pi has arrived, so that Pi does not queue behind them.
-//   prologue  wave 0: q^ = Pi RoPE(q) and u = S q^ (u = q^ for the
-//             per-element residual form). Rotating the query once replaces
-//             the per-key inverse rotation of Algorithm 1 (identical by
-//             Eq. 4). For a decode step (quantize-then-attend) waves 1 and 2
-//             meanwhile quantize the new key and value into the cache with the
-//             wave-per-vector quantizer of the append kernel, on the same
-//             staged Pi and S; the block whose tiles include the new token
-//             substitutes its codes in the registers of that tile instead of
-//             reading them back. Then two LDS tables per unit: a pair table
+//             through scalar loads.
+//   prologue  q^ = Pi RoPE(q) and u = S q^ (u = q^ for the per-element
+//             residual form), by all waves: 8 lanes per row of Pi, summed by
+//             DPP. Rotating the query once replaces the per-key inverse
+//             rotation of Algorithm 1 (identical by Eq. 4). Then two LDS
+//             tables per unit: a pair table
 //               T_A[p][a + 8 b] = q^_{2p} c_K[a] + q^_{2p+1} c_K[b]
 //             (one read scores two dimensions' table terms) and a sign table
 //               T_B[w][s] = sum_j u_{8w+j} (2 s_j - 1)
 //             over the 8 sign bits s of key word w (one read per word for the
-//             QJL term).
+//             QJL term). Only then are the block's tiles requested: a block
+//             that starts later on the same compute unit then finds its own
+//             Pi copy ahead of them in the memory pipeline.
+//   step      for a decode step (quantize-then-attend) waves 1 and 2 then
+//             quantize the new key and value into the cache with the append
+//             kernel's wave-per-vector quantizer on the staged Pi and S, while
+//             the other waves score; the wave that scores the new token's
+//             tile waits for them and substitutes the new codes in the
+//             registers of that tile (loaded before the append wrote them).
 //   main loop keys are scored one lane per token from the key words (3-bit
 //             indices in bits 0-23, signs in bits 24-31):
 //             score = n_k/8 (sum T_A + coef sum T_B), coef = alpha g_k (QJL) or
@@ -49,6 +52,7 @@ namespace tq {
 
 constexpr float kLazyRescale = 8.0f;   // log2 headroom before the max is raised
 constexpr int kXcds = 8;
+constexpr int kSpin = 1 << 22;     // bound of a wait on an LDS count (never reached)
 
 // Block barrier that orders LDS only. __syncthreads() also waits for every
 // outstanding global load of the wave (its release fence covers global
@@ -337,15 +341,17 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   constexpr int COLS = kDim / WAVES;       // rows of Pi per thread in the epilogue
   constexpr int DEPTH = 2;                 // tiles in flight per wave
   constexpr int MCH = 1024 / NT;           // 16-byte chunks of a 64 x 64 matrix per thread
-  constexpr int NB = 4;                    // read batch of the prologue's row products
+  constexpr int NB = 2;                    // read batch of the append's row products
   __shared__ __attribute__((aligned(16))) float s_pi[kDim * kDim];   // Pi (Swz16)
-  // S (Swz16) in the prologue; after the main loop the merge's scratch
+  // S (Swz16) in the prologue and a step's append; after the main loop the
+  // merge's scratch
   __shared__ __attribute__((aligned(16))) float s_ws[kDim * kDim];
   __shared__ __attribute__((aligned(16))) float s_ta[32 * 64];        // pair table of the score's table term
   __shared__ __attribute__((aligned(16))) float s_tb[8 * 256];        // sign-byte table of the QJL term
   // RoPE(q), q^, u, and the staging vectors x, r of the key and value appends
   __shared__ __attribute__((aligned(16))) float s_vec[7][kDim];
   __shared__ uint32_t s_new[2 + 8 + kDim];                           // the appended token's codes
+  __shared__ int s_ready;                                            // appends done
   __shared__ float s_vtab[16];
   __shared__ float s_wm[WAVES], s_wl[WAVES];
   __shared__ int s_last;
@@ -473,58 +479,57 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   const int64_t tile0 = s0 >> 6;
 
   // Pi and S have arrived (every wave waits for its own copies, then the
-  // barrier). Only now are the tiles requested: by the waves without
-  // prologue work at once, by the others when it is done (their registers
-  // then hold no tiles during the prologue).
+  // barrier).
+  if (t == 0) s_ready = 0;
   __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0)
   lds_barrier();
 
   // -------------------------------------------------------------- prologue
+  // q' = RoPE(q) (wave 0, one element per lane), then q^ = Pi q' and u = S q^
+  // by all waves: 8 lanes per row, 8 columns each, summed by DPP.
   if (wave == 0) {
     const float xin = f16 ? half_bits_to_float(xraw) : __uint_as_float(xraw);
     s_vec[0][lane] = rope_wave(xin, cs, half, lane);
-    wave_sync_lds();
-    const float qh = row_dot<Swz16, NB>(s_pi, s_vec[0], lane);
-    s_vec[1][lane] = qh;
-    float u = qh;
-    if (use_s) {
-      wave_sync_lds();
-      u = row_dot<Swz16, NB>(s_ws, s_vec[1], lane);
-    }
-    s_vec[2][lane] = u;
-  } else if (app && wave <= 2) {
-    const bool is_v = wave == 2;
-    const int ksign = paper ? 2 : 1;
-    const int sign_mode = is_v ? ((flags & kVQjl) ? ksign : 0) : ksign;
-    const bool rotate = !is_v || (flags & kVRotate);
-    const Lut8& c = is_v ? cvl : ck;
-    Levels La;
-    La.c0 = c.c0; La.c1 = c.c1; La.c2 = c.c2; La.c3 = c.c3;
-    La.c4 = c.c4; La.c5 = c.c5; La.c6 = c.c6; La.c7 = c.c7;
-    La.t0 = 0.5f * (La.c0 + La.c1); La.t1 = 0.5f * (La.c1 + La.c2); La.t2 = 0.5f * (La.c2 + La.c3);
-    La.t3 = 0.5f * (La.c3 + La.c4); La.t4 = 0.5f * (La.c4 + La.c5); La.t5 = 0.5f * (La.c5 + La.c6);
-    La.t6 = 0.5f * (La.c6 + La.c7);
-    const float xin = f16 ? half_bits_to_float(xraw) : __uint_as_float(xraw);
-    const float xr = is_v ? xin : rope_wave(xin, cs, half, lane);
-    const Appended ap = append_wave<Swz16, NB>(
-        xr, is_v, rotate, La, s_pi, s_ws, s_vec[is_v ? 5 : 3], s_vec[is_v ? 6 : 4], sign_mode, s0 + (n - 1),
-        lh, const_cast<uint8_t*>(a.k_codes), const_cast<uint8_t*>(a.v_codes),
-        const_cast<uint16_t*>(a.scalars), a.slots, lane);
-    if (!is_v) {
-      if ((lane & 7) == 0) s_new[2 + (lane >> 3)] = ap.code;
-      if (lane == 0) s_new[0] = ap.scal;
-    } else {
-      s_new[10 + lane] = ap.code;
-      if (lane == 0) s_new[1] = ap.scal;
-    }
   }
-  TileRegs buf[DEPTH];
+  lds_barrier();
+  const int prow = t >> 3, pc = t & 7;     // NT = 512: rows 0..63 (WAVES == 8); NT = 256: two passes
 #pragma unroll
-  for (int d = 0; d < DEPTH; ++d) {
-    const int tq = min(tile_begin + wave + d * WAVES, tile_end - 1);   // (a wave without tiles re-reads one)
-    load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
+  for (int r0 = 0; r0 < kDim; r0 += NT / 8) {
+    const int r = r0 + prow;
+    const float4* m4 = reinterpret_cast<const float4*>(s_pi);
+    const float4* x4 = reinterpret_cast<const float4*>(s_vec[0]);
+    const float4 ma = m4[Swz16::chunk(r, 2 * pc)], mb = m4[Swz16::chunk(r, 2 * pc + 1)];
+    const float4 xa = x4[2 * pc], xb = x4[2 * pc + 1];
+    float acc = ma.x * xa.x;
+    acc = fmaf(ma.y, xa.y, acc); acc = fmaf(ma.z, xa.z, acc); acc = fmaf(ma.w, xa.w, acc);
+    acc = fmaf(mb.x, xb.x, acc); acc = fmaf(mb.y, xb.y, acc); acc = fmaf(mb.z, xb.z, acc);
+    acc = fmaf(mb.w, xb.w, acc);
+    acc += dpp<0xB1>(acc);                 // quad_perm [1,0,3,2]
+    acc += dpp<0x4E>(acc);                 // quad_perm [2,3,0,1]
+    acc += dpp<0x141>(acc);                // row_half_mirror: the 8 lanes of the row
+    if (pc == 0) s_vec[1][r] = acc;
   }
-  lds_barrier();                           // q^, u (and the new token's codes) ready; S no longer read
+  lds_barrier();
+#pragma unroll
+  for (int r0 = 0; r0 < kDim; r0 += NT / 8) {
+    const int r = r0 + prow;
+    float acc = s_vec[1][r];
+    if (use_s) {
+      const float4* m4 = reinterpret_cast<const float4*>(s_ws);
+      const float4* x4 = reinterpret_cast<const float4*>(s_vec[1]);
+      const float4 ma = m4[Swz16::chunk(r, 2 * pc)], mb = m4[Swz16::chunk(r, 2 * pc + 1)];
+      const float4 xa = x4[2 * pc], xb = x4[2 * pc + 1];
+      acc = ma.x * xa.x;
+      acc = fmaf(ma.y, xa.y, acc); acc = fmaf(ma.z, xa.z, acc); acc = fmaf(ma.w, xa.w, acc);
+      acc = fmaf(mb.x, xb.x, acc); acc = fmaf(mb.y, xb.y, acc); acc = fmaf(mb.z, xb.z, acc);
+      acc = fmaf(mb.w, xb.w, acc);
+      acc += dpp<0xB1>(acc);
+      acc += dpp<0x4E>(acc);
+      acc += dpp<0x141>(acc);
+    }
+    if (pc == 0) s_vec[2][r] = acc;
+  }
+  lds_barrier();
 
   // Table entries built by this thread (NT threads):
   //   ta (2048 entries): e = t + NT m, pair P = e / 64 = wave + WAVES m, index f = e % 64 = lane
@@ -557,6 +562,49 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   }
   lds_barrier();
 
+  // ------------------------------------------------------------ step append
+  // For a decode step, waves 1 and 2 quantize the new key and value into the
+  // cache (with the append kernel's quantizer, on the staged Pi and S) while
+  // the other waves start scoring; each raises the count in s_ready when its
+  // codes are in s_new. The wave that scores the new token's tile waits for
+  // both before it does (bounded: the appends never wait on anything).
+  if (app && (wave == 1 || wave == 2)) {
+    const bool is_v = wave == 2;
+    const int ksign = paper ? 2 : 1;
+    const int sign_mode = is_v ? ((flags & kVQjl) ? ksign : 0) : ksign;
+    const bool rotate = !is_v || (flags & kVRotate);
+    const Lut8& c = is_v ? cvl : ck;
+    Levels La;
+    La.c0 = c.c0; La.c1 = c.c1; La.c2 = c.c2; La.c3 = c.c3;
+    La.c4 = c.c4; La.c5 = c.c5; La.c6 = c.c6; La.c7 = c.c7;
+    La.t0 = 0.5f * (La.c0 + La.c1); La.t1 = 0.5f * (La.c1 + La.c2); La.t2 = 0.5f * (La.c2 + La.c3);
+    La.t3 = 0.5f * (La.c3 + La.c4); La.t4 = 0.5f * (La.c4 + La.c5); La.t5 = 0.5f * (La.c5 + La.c6);
+    La.t6 = 0.5f * (La.c6 + La.c7);
+    const float xin = f16 ? half_bits_to_float(xraw) : __uint_as_float(xraw);
+    const float xr = is_v ? xin : rope_wave(xin, cs, half, lane);
+    const Appended ap = append_wave<Swz16, NB>(
+        xr, is_v, rotate, La, s_pi, s_ws, s_vec[is_v ? 5 : 3], s_vec[is_v ? 6 : 4], sign_mode, s0 + (n - 1),
+        lh, const_cast<uint8_t*>(a.k_codes), const_cast<uint8_t*>(a.v_codes),
+        const_cast<uint16_t*>(a.scalars), a.slots, lane);
+    if (!is_v) {
+      if ((lane & 7) == 0) s_new[2 + (lane >> 3)] = ap.code;
+      if (lane == 0) s_new[0] = ap.scal;
+    } else {
+      s_new[10 + lane] = ap.code;
+      if (lane == 0) s_new[1] = ap.scal;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");   // s_new written (LDS only)
+    if (lane == 0) __hip_atomic_fetch_add(&s_ready, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  // Tiles are requested only now (the appending waves' registers hold no
+  // tiles through the append).
+  TileRegs buf[DEPTH];
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) {
+    const int tq = min(tile_begin + wave + d * WAVES, tile_end - 1);   // (a wave without tiles re-reads one)
+    load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
+  }
+
   // -------------------------------------------------------------- main loop
   float m_run = -INFINITY;
   float l_lane = 0.0f;
@@ -570,7 +618,14 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     for (int d = 0; d < DEPTH; ++d) {
       const int tt = tb + d * WAVES;
       if (tt >= tile_end) break;
-      if (app && tt == tnew) patch_new_token(buf[d], s_new, rnew, lane);
+      if (app && tt == tnew) {
+        for (int i = 0; i < kSpin; ++i) {
+          if (__hip_atomic_load(&s_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= 2) break;
+          __builtin_amdgcn_s_sleep(1);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        patch_new_token(buf[d], s_new, rnew, lane);
+      }
       const TileRegs& cur = buf[d];
       const int tok = tt * kTile + lane;
       const bool tv = tok < n;
@@ -633,9 +688,12 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   }
 
   // ------------------------------------------------------ merge the waves
+  // (s_wo shares its LDS with S, which a step's key append may still be
+  // reading until every wave has come here)
   const float ov = (o0 + o1) + (o2 + o3);
   const float l_wave = wave_sum_uniform(l_lane);
   if (lane == 0) { s_wm[wave] = m_run; s_wl[wave] = l_wave; }
+  lds_barrier();
   s_wo[wave * kDim + lane] = ov;
   if (VQJL) s_wsg[wave * kDim + lane] = sg;
   __syncthreads();
