@@ -3,9 +3,9 @@
 Workload (default "esm2-650m-33layer-seq1024"): 33 layers x 20 heads x 64,
 batch 1, 1024 cached tokens, fp16 I/O, synthetic seeded inputs. One step =
 tq_decode_step over all 33 layers: append the new token (RoPE, rotation,
-3-bit codes, QJL signs, packing) and attend over the 1025 cached tokens, as
-two kernel launches (a step prologue that rotates the query and quantizes
-the new key and value with one read of each Pi, then the attention kernel).
+3-bit codes, QJL signs, packing) and attend over the 1025 cached tokens, in
+one kernel launch (decode_kernel: each (layer, head) block reads its Pi
+once, rotates the query, quantizes the new key and value, and attends).
 Steps rotate over replicas of every per-step input (cache, Pi, query, new
 token) totalling >= 1 GiB, so each step reads its data from HBM rather than
 from the 256 MB Infinity Cache. The K timed steps are captured in one HIP
@@ -261,8 +261,9 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                      "traffic_source": traffic_src,
-                     "kernel": ("decode_attend: prep + attention kernels" if args.decode_only else
-                                "decode_step: step prologue + attention kernels"),
+                     "kernel": ("decode_kernel<8, false> (one launch per tq_decode_attend call)"
+                                if args.decode_only else
+                                "decode_kernel<8, false> (one launch per tq_decode_step call)"),
                      "alg_bytes_per_launch": int(alg_bytes)},
         "cpu_baseline": cpu,
         "fp16_attention_baseline": fp16_base,
