@@ -32,7 +32,7 @@
 //             raised only when a tile max exceeds it by more than 2^8.
 //             Values are accumulated one lane per dimension from the
 //             dimension-major V tile; a tile's token weights reach the lanes
-//             through DPP row broadcasts. Two tiles per wave are in flight.
+//             through DPP row broadcasts. One tile per wave is in flight (two with 4 waves).
 //   merge     waves merge through LDS; splits of a unit merge through a
 //             workspace of (m, l, o) partials written and read with
 //             agent-scope atomics: the last split to finish (atomic counter)
@@ -339,7 +339,9 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   constexpr int TAM = 2048 / NT;           // pair-table entries per thread
   constexpr int TBM = 512 / NT;            // groups of 4 sign-table entries per thread
   constexpr int COLS = kDim / WAVES;       // rows of Pi per thread in the epilogue
-  constexpr int DEPTH = 2;                 // tiles in flight per wave
+  // tiles in flight per wave: with 8 waves one (more only queue ahead of
+  // the Pi copies of blocks that start later on the compute unit)
+  constexpr int DEPTH = WAVES == 8 ? 1 : 2;
   constexpr int MCH = 1024 / NT;           // 16-byte chunks of a 64 x 64 matrix per thread
   constexpr int NB = 2;                    // read batch of the append's row products
   __shared__ __attribute__((aligned(16))) float s_pi[kDim * kDim];   // Pi (Swz16)
