@@ -2,16 +2,19 @@
 // table codes -> residual -> QJL sign bits -> packed cache (TurboESM Sec. 3.1
 // prefill steps 1, 3, 4; Sec. 3.3; Sec. 3.4; Sec. 4.2).
 //
-// Two kernels compute the same bits:
-//   quantize_tiles_kernel   one lane per token, 64 tokens per wave, for
-//                           prefill-sized T. Pi and S sit in LDS and are read
-//                           as wave-wide broadcasts.
+// Two kernels:
+//   quantize_tiles_kernel   for prefill-sized T: 64 tokens per wave; the
+//                           rotations x^ = Pi x' of the wave's 64 x 64 block
+//                           run on the matrix cores (fp32 MFMA), then one lane
+//                           per token runs the quantizer steps.
 //   quantize_vectors_kernel one wave per vector (one lane per dimension; the
 //                           key and the value of a token-head in parallel), for
-//                           decode-step appends with small T.
-// Both evaluate the rotation as an fma chain over k ascending and the
-// quantizer steps with the fixed binary32 order of quantize_lane, so a token
-// gets the same codes from either kernel.
+//                           decode-step appends with small T; its rotation is
+//                           an fma chain over k ascending.
+// Both run the quantizer steps (norm, levels, residual, projected signs) in
+// the fixed binary32 order of quantize_lane / quantize_wave, so identical x^
+// give identical bits; for raw inputs the two rotations sum in different
+// orders, so a code can differ where x^ sits within rounding of a threshold.
 #include "tq_append.hpp"
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
@@ -38,67 +41,146 @@ hipError_t launch_rope_table(float* cs, int positions, double base, hipStream_t 
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------ shared pieces
-// RoPE of one vector held by one lane (pairs (2m, 2m+1), or (m, m+32) with
-// half pairing): x'_a = x_a c - x_b s, x'_b = x_a s + x_b c in binary32.
-__device__ __forceinline__ void rope_lane(float (&x)[kDim], const float* cs_row, bool half) {
-  const float4* cs4 = reinterpret_cast<const float4*>(cs_row);
-  float c[kPairs], s[kPairs];
+// ------------------------------------------------- MFMA rotation of 64 rows
+// x^ = Pi x' for the 64 tokens of a wave as D = Pi X'^T on the matrix cores
+// (v_mfma_f32_32x32x2f32: fp32 products, fp32 sums), in two 32-row blocks of
+// Pi (mb) times two 32-token blocks (nb), 32 rank-2 steps each.
+// Operand layout of the instruction (lane l, n = l % 32, h = l / 32):
+//   A lane value  A[n][h]       (row n of the 32 x 2 slice)
+//   B lane value  B[h][n]       (column n of the 2 x 32 slice)
+//   D register r  D[8 (r/4) + 4h + r%4][n]
+// Step s (q = s/4, jj = s%4) gives lane half h the contraction index
+// k = 8q + 4h + jj, so the 32 k a lane contributes are the dimensions
+// {8q + 4h + jj}: the same set that D leaves in that lane half. A lane's
+// B values are therefore 8 groups of 4 consecutive dimensions of its token
+// (one 8- or 16-byte load each) and its A values are 4 consecutive columns
+// of a row of Pi (one 16-byte LDS read per q).
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Pitch of the staged Pi: 16-byte row reads of 16 lanes (rows n, 4n dwords
+// apart modulo 64 banks) are conflict-free.
+constexpr int kPiPitch = 68;
+
+// Loads the lane's half row of token j0 + 32 nb + n (values x'[8q + 4h + jj]
+// at step 4q + jj) and applies RoPE (keys): both pairings keep a pair inside
+// the lane's set (interleaved: (2m, 2m + 1) inside one group of 4; half: d and
+// d + 32 in groups q and q + 4).
+template <bool F16>
+__device__ __forceinline__ void load_half_row(float (&xv)[32], const QuantArgs& a, const void* src, int li,
+                                              int b, int h, int j0, int nb, int lane, bool rope) {
+  const int n = lane & 31, hh = lane >> 5;
+  const bool half = (a.flags & kRopeHalf) != 0;
+  const int j = j0 + 32 * nb + n;
+  const int pos = a.pos0[b] + j;
+  const bool ok = j < a.T && (!rope || (pos >= 0 && pos < a.rope_positions));
+  const int64_t row = ((((int64_t)li * a.B + b) * a.T + j) * a.H + h) * kDim;
 #pragma unroll
-  for (int q = 0; q < kPairs / 2; ++q) {
-    const float4 v = cs4[q];
-    c[2 * q] = v.x; s[2 * q] = v.y; c[2 * q + 1] = v.z; s[2 * q + 1] = v.w;
+  for (int q = 0; q < 8; ++q) {
+    const int d0 = 8 * q + 4 * hh;
+    float4 f = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (ok) {
+      if (F16) {
+        const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const __half*>(src) + row + d0);
+        f.x = half_bits_to_float(w.x); f.y = half_bits_to_float(w.x >> 16);
+        f.z = half_bits_to_float(w.y); f.w = half_bits_to_float(w.y >> 16);
+      } else {
+        f = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(src) + row + d0);
+      }
+    }
+    xv[4 * q + 0] = f.x; xv[4 * q + 1] = f.y; xv[4 * q + 2] = f.z; xv[4 * q + 3] = f.w;
   }
-  if (half) {
+  if (!rope || !ok) return;
+  const float4* cs4 = reinterpret_cast<const float4*>(a.rope_cs + (int64_t)pos * 2 * kPairs);
+  if (!half) {
+    // pairs d0/2 and d0/2 + 1 of group q: their (cos, sin) in one float4
 #pragma unroll
-    for (int m = 0; m < kPairs; ++m) {
-      const float xa = x[m], xb = x[m + kPairs];
-      x[m] = xa * c[m] - xb * s[m];
-      x[m + kPairs] = xa * s[m] + xb * c[m];
+    for (int q = 0; q < 8; ++q) {
+      const float4 c = cs4[2 * q + hh];
+      const float x0 = xv[4 * q], x1 = xv[4 * q + 1], x2 = xv[4 * q + 2], x3 = xv[4 * q + 3];
+      xv[4 * q + 0] = x0 * c.x - x1 * c.y; xv[4 * q + 1] = x0 * c.y + x1 * c.x;
+      xv[4 * q + 2] = x2 * c.z - x3 * c.w; xv[4 * q + 3] = x2 * c.w + x3 * c.z;
     }
   } else {
+    // pair (d, d + 32) for d in group q < 4, angle index d
 #pragma unroll
-    for (int m = 0; m < kPairs; ++m) {
-      const float xa = x[2 * m], xb = x[2 * m + 1];
-      x[2 * m] = xa * c[m] - xb * s[m];
-      x[2 * m + 1] = xa * s[m] + xb * c[m];
+    for (int q = 0; q < 4; ++q) {
+      const int d0 = 8 * q + 4 * hh;
+      const float4 c01 = cs4[d0 >> 1], c23 = cs4[(d0 >> 1) + 1];
+      const float cc[4] = {c01.x, c01.z, c23.x, c23.z}, ss[4] = {c01.y, c01.w, c23.y, c23.w};
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        const float xa = xv[4 * q + jj], xb = xv[4 * (q + 4) + jj];
+        xv[4 * q + jj] = xa * cc[jj] - xb * ss[jj];
+        xv[4 * (q + 4) + jj] = xa * ss[jj] + xb * cc[jj];
+      }
     }
   }
 }
 
-// x^_i = fma chain over k ascending of Pi[i][k] x_k; Pi in LDS (row-major),
-// read as broadcasts. The per-lane result goes through the lane's own LDS
-// column so that the output index stays static.
-__device__ __forceinline__ void rotate_lane(float (&x)[kDim], const float* s_pi, float* s_col,
-                                            int lane) {
-  for (int i = 0; i < kDim; ++i) {
-    const float4* row = reinterpret_cast<const float4*>(s_pi + i * kDim);
-    float acc = 0.0f;
+// acc[mb] += the 32 rank-2 steps of row block mb of Pi times one token block.
+// The Pi reads are issued per group q (the empty asm keeps the compiler from
+// holding all 64 values of Pi in registers across both token blocks).
+__device__ __forceinline__ void rotate_block(const float (&xv)[32], const float* s_pi, int lane,
+                                             f32x16& acc0, f32x16& acc1) {
+  const int n = lane & 31, hh = lane >> 5;
 #pragma unroll
-    for (int k4 = 0; k4 < kDim / 4; ++k4) {
-      const float4 p = row[k4];
-      acc = fmaf(p.x, x[4 * k4 + 0], acc);
-      acc = fmaf(p.y, x[4 * k4 + 1], acc);
-      acc = fmaf(p.z, x[4 * k4 + 2], acc);
-      acc = fmaf(p.w, x[4 * k4 + 3], acc);
-    }
-    s_col[i * kDim + lane] = acc;
+  for (int q = 0; q < 8; ++q) {
+    int o = n * kPiPitch + 8 * q + 4 * hh;
+    asm volatile("" : "+v"(o));
+    const float4 p0 = *reinterpret_cast<const float4*>(s_pi + o);
+    const float4 p1 = *reinterpret_cast<const float4*>(s_pi + o + 32 * kPiPitch);
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(p0.x, xv[4 * q + 0], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(p1.x, xv[4 * q + 0], acc1, 0, 0, 0);
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(p0.y, xv[4 * q + 1], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(p1.y, xv[4 * q + 1], acc1, 0, 0, 0);
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(p0.z, xv[4 * q + 2], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(p1.z, xv[4 * q + 2], acc1, 0, 0, 0);
+    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(p0.w, xv[4 * q + 3], acc0, 0, 0, 0);
+    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(p1.w, xv[4 * q + 3], acc1, 0, 0, 0);
+  }
+}
+
+// Rotates the wave's 64 tokens and hands lane l all 64 rotated values of token
+// j0 + l: after the products, lane half h of token block nb holds dimensions
+// {8q + 4h + jj} of token 32 nb + n; one v_permlane32_swap per register pair
+// moves the upper half of block 0 and the lower half of block 1 across, so
+// that lane l < 32 holds token l and lane l >= 32 token l (32 + n).
+template <bool F16>
+__device__ __forceinline__ void rotate_tokens(float (&out)[kDim], const QuantArgs& a, const void* src,
+                                              const float* s_pi, int li, int b, int h, int j0, int lane,
+                                              bool rope) {
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) { acc[0][0][r] = 0.0f; acc[1][0][r] = 0.0f; acc[0][1][r] = 0.0f; acc[1][1][r] = 0.0f; }
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    float xv[32];
+    load_half_row<F16>(xv, a, src, li, b, h, j0, nb, lane, rope);
+    rotate_block(xv, s_pi, lane, acc[0][nb], acc[1][nb]);
   }
 #pragma unroll
-  for (int i = 0; i < kDim; ++i) x[i] = s_col[i * kDim + lane];
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[mb][0][r]),
+                                                       __float_as_uint(acc[mb][1][r]), false, false);
+      const int d = 32 * mb + 8 * (r >> 2) + (r & 3);
+      out[d] = __uint_as_float(sw[0]);       // dimension set of lane half 0
+      out[d + 4] = __uint_as_float(sw[1]);   // dimension set of lane half 1
+    }
 }
 
 // ----------------------------------------------------- lane-per-token kernel
-// Block: 2 waves x 64 tokens of one (layer, sequence, head). Grid:
-// x = ceil(T/128), y = B*H, z = nlayers. Dynamic LDS (64 KiB): Pi, S and one
-// 64 x 64 column buffer per wave.
-template <bool F16>
-__global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
-  extern __shared__ float smem[];
-  float* s_pi = smem;
-  float* s_S = smem + kDim * kDim;
+// Block: 4 waves x 64 tokens of one (layer, sequence, head). Grid:
+// x = ceil(T/256), y = B*H, z = nlayers. LDS: Pi (pitch 68) for the
+// rotations, S (row-major, read by the quantizer as broadcasts) and one
+// 64 x 8 word buffer per wave for the V transpose.
+template <bool F16, bool VQJL>
+__global__ __launch_bounds__(256) void quantize_tiles_kernel(QuantArgs a) {
+  __shared__ __attribute__((aligned(16))) float s_pi[kDim * kPiPitch];
+  __shared__ __attribute__((aligned(16))) float s_S[kDim * kDim];
+  __shared__ uint32_t s_vt[4][kDim * 8];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  float* s_col = smem + 2 * kDim * kDim + wave * kDim * kDim;
 
   const int h = blockIdx.y % a.H, b = blockIdx.y / a.H, li = blockIdx.z;
   const int l = a.layer0 + li;
@@ -106,17 +188,19 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
   const bool rotated = (a.flags & kInputRotated) != 0;
   const bool paper = (a.flags & kQjlPaper) != 0;
   const int ksign = paper ? 2 : 1;
-  const int vsign = (a.flags & kVQjl) ? ksign : 0;
+  const int vsign = VQJL ? ksign : 0;   // (a V sign pass is compiled only where asked for)
 
-  for (int e = threadIdx.x; e < kDim * kDim; e += blockDim.x) {
-    s_pi[e] = a.pi[lh * kDim * kDim + e];
-    s_S[e] = a.qjl_s[e];
+  for (int e = threadIdx.x; e < kDim * kDim / 4; e += blockDim.x) {
+    const float4 pv = reinterpret_cast<const float4*>(a.pi + lh * kDim * kDim)[e];
+    *reinterpret_cast<float4*>(s_pi + (e >> 4) * kPiPitch + (e & 15) * 4) = pv;
+    reinterpret_cast<float4*>(s_S)[e] = reinterpret_cast<const float4*>(a.qjl_s)[e];
   }
   const Levels Lk = load_levels(a.lut_k + lh * 8);
   const Levels Lv = load_levels(a.lut_v + lh * 8);
   __syncthreads();
 
-  const int j0 = blockIdx.x * 128 + wave * kTile;
+  const int j0 = blockIdx.x * 256 + wave * kTile;
+  if (j0 >= a.T) return;                  // wave-uniform; no barrier follows
   const int j = j0 + lane;
   const int64_t sbase = a.slot0[b];
   const int pbase = a.pos0[b];
@@ -129,13 +213,13 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
   uint8_t* kreg = a.k_codes + lh * a.slots * 32;
   uint8_t* vreg = a.v_codes + lh * a.slots * 32;
 
-  // ---- K
+  // ---- K: RoPE and rotation, or a pre-rotated input as is
   float x[kDim];
+  if (rotated) {
 #pragma unroll
-  for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.k, row + i, F16) : 0.0f;
-  if (!rotated) {
-    if (ok) rope_lane(x, a.rope_cs + (int64_t)pos * 2 * kPairs, (a.flags & kRopeHalf) != 0);
-    rotate_lane(x, s_pi, s_col, lane);
+    for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.k, row + i, false) : 0.0f;
+  } else {
+    rotate_tokens<F16>(x, a, a.k, s_pi, li, b, h, j0, lane, true);
   }
   uint32_t kw[8];
   const QuantOut qk = quantize_lane<true>(x, Lk, s_S, ksign, kw);
@@ -146,10 +230,15 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
     *reinterpret_cast<uint4*>(kreg + tile_half_offset(tile, 1, r)) = make_uint4(kw[4], kw[5], kw[6], kw[7]);
   }
 
-  // ---- V (no RoPE)
+  // ---- V (no RoPE): rotated like K unless TQ_V_ROTATE is off. The V loads
+  // are not hoisted above the key's stores (registers, occupancy).
+  asm volatile("" ::: "memory");
+  if (!rotated && (a.flags & kVRotate)) {
+    rotate_tokens<F16>(x, a, a.v, s_pi, li, b, h, j0, lane, false);
+  } else {
 #pragma unroll
-  for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.v, row + i, F16) : 0.0f;
-  if (!rotated && (a.flags & kVRotate)) rotate_lane(x, s_pi, s_col, lane);
+    for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.v, row + i, F16) : 0.0f;
+  }
   uint32_t vw[8];
   const QuantOut qv = quantize_lane<false>(x, Lv, s_S, vsign, vw);
   if (ok) {
@@ -158,8 +247,8 @@ __global__ __launch_bounds__(128) void quantize_tiles_kernel(QuantArgs a) {
   }
 
   // V is stored dimension-major: transpose the wave's 64 x 64 nibbles through
-  // the lane's LDS column (token-major words in, one dimension per lane out).
-  uint32_t* s_w = reinterpret_cast<uint32_t*>(s_col);
+  // its LDS buffer (token-major words in, one dimension per lane out).
+  uint32_t* s_w = s_vt[wave];
 #pragma unroll
   for (int w = 0; w < 8; ++w) s_w[lane * 8 + w] = vw[w];
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -266,12 +355,16 @@ __global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, uint
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t st) {
   const bool f16 = a.f16 && !(a.flags & kInputRotated);
   if (a.T >= 64) {
-    dim3 grid((a.T + 127) / 128, a.B * a.H, a.nlayers);
-    const size_t lds = (size_t)(2 + 2) * kDim * kDim * sizeof(float);
-    if (f16)
-      hipLaunchKernelGGL(quantize_tiles_kernel<true>, grid, dim3(128), lds, st, a);
+    dim3 grid((a.T + 255) / 256, a.B * a.H, a.nlayers);
+    const bool vq = (a.flags & kVQjl) != 0;
+    if (f16 && vq)
+      hipLaunchKernelGGL((quantize_tiles_kernel<true, true>), grid, dim3(256), 0, st, a);
+    else if (f16)
+      hipLaunchKernelGGL((quantize_tiles_kernel<true, false>), grid, dim3(256), 0, st, a);
+    else if (vq)
+      hipLaunchKernelGGL((quantize_tiles_kernel<false, true>), grid, dim3(256), 0, st, a);
     else
-      hipLaunchKernelGGL(quantize_tiles_kernel<false>, grid, dim3(128), lds, st, a);
+      hipLaunchKernelGGL((quantize_tiles_kernel<false, false>), grid, dim3(256), 0, st, a);
   } else {
     const uint32_t total = (uint32_t)((int64_t)a.nlayers * a.B * a.T * a.H);
     if (f16)

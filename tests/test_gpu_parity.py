@@ -87,24 +87,6 @@ def test_quantize_bit_exact_on_rotated_inputs(T, B, slot0, flags):
     assert oc.s.any()
 
 
-def test_quantize_kernels_agree_on_raw_inputs():
-    # The tile kernel (T >= 64) and the wave kernel (T < 64) rotate in the
-    # same fma order, so they must write identical bytes for the same tokens.
-    L, H, T = 1, 4, 64
-    case = Case(12, L, H, 1, T, io="f16", slots=128)
-    a = tq.Cache(L, H, 128)
-    case.gpu_quantize(a)
-    b = tq.Cache(L, H, 128)
-    for j0 in range(0, T, 16):
-        sl = slice(j0, j0 + 16)
-        case.gpu_quantize(b, k=case.t("k")[:, :, sl].contiguous(), v=case.t("v")[:, :, sl].contiguous(),
-                          pos0=[j0], slot0=[j0])
-    torch.cuda.synchronize()
-    assert torch.equal(a.k_codes, b.k_codes)
-    assert torch.equal(a.v_codes, b.v_codes)
-    assert torch.equal(a.scalars, b.scalars)
-
-
 def _threshold_distance(case, oc_flags, li, b, j, h, is_key):
     x = (case.k if is_key else case.v)[li, b, j, h].astype(np.float32)
     l = case.layer0 + li
@@ -117,30 +99,22 @@ def _threshold_distance(case, oc_flags, li, b, j, h, is_key):
     return np.min(np.abs(u[:, None] - t[None, :]), axis=1)
 
 
-@pytest.mark.parametrize("T", [256, 3])
-def test_quantize_end_to_end_matches_up_to_threshold_rounding(T):
-    L, H, B = 1, 8, 2
-    case = Case(13, L, H, B, T, io="f16", slots=2 * 320, slot0=[0, 320], pos0=[0, 17])
-    cache = tq.Cache(L, H, case.slots)
-    case.gpu_quantize(cache)
-    torch.cuda.synchronize()
-    oc = oracle.Cache(L, H, case.slots)
-    case.oracle_quantize(oc)
-    got = to_oracle(cache)
-    # norms: fp16 of binary32 norms of vectors that agree to ~1e-6
+def _assert_agree_up_to_threshold_rounding(case, got, ref, B, T, H):
+    """Two caches quantized from the same raw inputs by two binary32 paths
+    (RoPE and rotation summed in different orders): the fp16 norms agree to
+    one ulp and a code differs only where the exact coordinate sits within
+    rounding of a decision threshold, by one level."""
     ng = got.s.view(np.float16).astype(np.float64)
-    no = oc.s.view(np.float16).astype(np.float64)
+    no = ref.s.view(np.float16).astype(np.float64)
     assert np.all(np.abs(ng - no) <= fp16_ulp(no) + 1e-12)
-    code_diff = 0
-    sign_diff = 0
-    total = 0
+    code_diff = sign_diff = total = 0
     for b in range(B):
         for j in range(T):
             s = int(case.slot0[b]) + j
             for h in range(H):
                 for is_key, which in ((True, "k"), (False, "v")):
                     ng_ = oracle.unpack_slot(got.region(which, 0, h), s, which)
-                    no_ = oracle.unpack_slot(oc.region(which, 0, h), s, which)
+                    no_ = oracle.unpack_slot(ref.region(which, 0, h), s, which)
                     total += 64
                     bad = (ng_ & 7) != (no_ & 7)
                     sign_diff += int(((ng_ >> 3) != (no_ >> 3)).sum())
@@ -150,7 +124,38 @@ def test_quantize_end_to_end_matches_up_to_threshold_rounding(T):
                         assert np.all(dist[bad] < 1e-4), (b, j, h, which, dist[bad])
                         assert np.all(np.abs((ng_[bad] & 7).astype(int) - (no_[bad] & 7)) == 1)
     assert code_diff <= 1e-3 * total
+    # a sign bit follows the residual: it may flip with a code, or where its
+    # projection is within rounding of zero
     assert sign_diff <= 64 * code_diff + 1e-4 * total
+
+
+def test_quantize_kernels_agree_on_raw_inputs():
+    # The tile kernel (T >= 64, rotations on the matrix cores) and the wave
+    # kernel (T < 64, fma chains) sum the rotations in different orders: the
+    # codes they write for the same raw tokens agree up to threshold rounding.
+    L, H, T = 1, 4, 128
+    case = Case(12, L, H, 1, T, io="f16", slots=128)
+    a = tq.Cache(L, H, 128)
+    case.gpu_quantize(a)
+    b = tq.Cache(L, H, 128)
+    for j0 in range(0, T, 16):
+        sl = slice(j0, j0 + 16)
+        case.gpu_quantize(b, k=case.t("k")[:, :, sl].contiguous(), v=case.t("v")[:, :, sl].contiguous(),
+                          pos0=[j0], slot0=[j0])
+    torch.cuda.synchronize()
+    _assert_agree_up_to_threshold_rounding(case, to_oracle(a), to_oracle(b), 1, T, H)
+
+
+@pytest.mark.parametrize("T", [256, 3])
+def test_quantize_end_to_end_matches_up_to_threshold_rounding(T):
+    L, H, B = 1, 8, 2
+    case = Case(13, L, H, B, T, io="f16", slots=2 * 320, slot0=[0, 320], pos0=[0, 17])
+    cache = tq.Cache(L, H, case.slots)
+    case.gpu_quantize(cache)
+    torch.cuda.synchronize()
+    oc = oracle.Cache(L, H, case.slots)
+    case.oracle_quantize(oc)
+    _assert_agree_up_to_threshold_rounding(case, to_oracle(cache), oc, B, T, H)
 
 
 # --------------------------------------------------------------------- decode
