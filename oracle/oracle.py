@@ -7,7 +7,7 @@ library and never imports it.
 
 Contents
   C core (``tq_oracle.c``, loaded through ctypes):
-    rope_table, rotated_input, quantize_vector, quantize_pack, decode,
+    rope_table, rotated_input, quantize_vector, quantize_pack, decode, dequantize,
     f32_to_f16 / f16_to_f32, pack/unpack of one slot.
   NumPy / SciPy:
     lloyd_max_gaussian  3-bit Lloyd-Max levels for N(0, 1)     (Sec. 3.3, Eq. 5)
@@ -76,6 +76,8 @@ def lib():
                                         i32, i32, P, P, P, P, P, P, P, P, P]
         L.orc_decode.argtypes = [i32, i32, i64, u32, dbl, P, i32, P, i32, i32, i32,
                                  P, P, P, P, P, P, P, P, P, P, P, P, i64, i32, P]
+        L.orc_dequantize.argtypes = [i32, i32, i64, u32, i32, i32, i32, P, P, i32,
+                                     P, P, P, P, P, P, P, P, P]
         _lib = L
     return _lib
 
@@ -226,6 +228,29 @@ def decode(cache: Cache, flags: int, cs, q, q_pos, seq_slot0, seq_len, pi, lut_k
                      _p(units) if units is not None else None,
                      0 if units is None else len(units), int(twostep), _p(out))
     return out
+
+
+def dequantize(cache: Cache, flags: int, seq_slot0, seq_len, max_len: int, lut_k, lut_v, S,
+               ebar=None, layer0: int = 0, nl: int | None = None):
+    """The dequantized keys and values of every cached token (the first step of
+    a dequantize-then-attend path), fp64 [nl][B][H][max_len][64] each:
+    k~ = (n_k/8)(c_K[idx] + alpha g_k S^T(2s - 1)) (per-element form:
+    ebar_K (2s - 1)), v~ = (n_v/8)(c_V[idx] + the V residual estimate with
+    V_QJL), so that q^ . k~ is the decode score and v~ the decoded value.
+    Rows past a sequence's length (or of an invalid sequence) are NaN."""
+    s0 = np.ascontiguousarray(seq_slot0, dtype=np.int64)
+    sl = np.ascontiguousarray(seq_len, dtype=np.int32)
+    B = len(sl)
+    nl = cache.L - layer0 if nl is None else nl
+    H = cache.H
+    ko = np.full((nl, B, H, max_len, D), np.nan, dtype=np.float64)
+    vo = np.full((nl, B, H, max_len, D), np.nan, dtype=np.float64)
+    eb = _f32(ebar) if ebar is not None else None
+    lib().orc_dequantize(cache.L, H, cache.slots, int(flags), B, layer0, nl, _p(s0), _p(sl),
+                         int(max_len), _p(_f32(lut_k)), _p(_f32(lut_v)), _p(_f32(S)),
+                         _p(eb) if eb is not None else None, _p(cache.k), _p(cache.v), _p(cache.s),
+                         _p(ko), _p(vo))
+    return ko, vo
 
 
 # --------------------------------------------------------------------------

@@ -376,6 +376,26 @@ static void dequant_v(const uint8_t* nib, double nv, double gv, const double* cv
   for (int i = 0; i < D; ++i) out[i] *= nv / 8.0;
 }
 
+/* Dequantized key of one token, the form a "dequantize first, then attend"
+ * path materializes (Sec. 3.4 applied to a stored key rather than to a
+ * score): k~ = (n_k/8) (c_K[idx] + coef e) with e = S^T (2s - 1) and
+ * coef = alpha g_k for the projected estimator, or e = 2s - 1 and
+ * coef = ebar_K for the per-element form, so that q^ . k~ is key_score. */
+static void dequant_k(const uint8_t* nib, double nk, double gk, const double* ck,
+                      uint32_t flags, double ebar_k, const float* S, double* out) {
+  for (int i = 0; i < D; ++i) out[i] = ck[nib[i] & 7];
+  if (flags & F_QJL_PAPER) {
+    for (int i = 0; i < D; ++i) out[i] += ebar_k * ((nib[i] >> 3) ? 1.0 : -1.0);
+  } else {
+    for (int kk = 0; kk < D; ++kk) {
+      double acc = 0.0;
+      for (int i = 0; i < D; ++i) acc += (double)S[i * D + kk] * ((nib[i] >> 3) ? 1.0 : -1.0);
+      out[kk] += ALPHA * gk * acc;
+    }
+  }
+  for (int i = 0; i < D; ++i) out[i] *= nk / 8.0;
+}
+
 /* Attention score of one cached key against the rotated query:
  * (n_k/8) ( sum_i q^_i c_K[idx_i] + coef sum_i y_i (2 s_i - 1) ),
  * coef = alpha g_k, y = S q^ (projected QJL), or coef = ebar_K, y = q^. */
@@ -518,5 +538,46 @@ void orc_decode(int L, int H, int64_t slots, uint32_t flags, double scale,
     else
       decode_unit_streaming(&u, flags, scale, kc + region * 32, vc + region * 32,
                             sc + region * 4, s0, n, P, S, o);
+  }
+}
+
+/* Dequantize every cached token of the units (li, b, h): k_out, v_out are
+ * [nl][B][H][max_len][64] doubles; rows j < seq_len[b] of a valid sequence
+ * are written, the rest are left as they are. */
+void orc_dequantize(int L, int H, int64_t slots, uint32_t flags, int B, int layer0, int nl,
+                    const int64_t* sslot0, const int32_t* slen, int max_len,
+                    const float* lut_k, const float* lut_v, const float* S, const float* ebar,
+                    const uint8_t* kc, const uint8_t* vc, const uint16_t* sc,
+                    double* k_out, double* v_out) {
+  (void)L;
+  int64_t total = (int64_t)nl * B * H;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t t = 0; t < total; ++t) {
+    int h = (int)(t % H);
+    int b = (int)((t / H) % B);
+    int li = (int)(t / ((int64_t)H * B));
+    int l = layer0 + li;
+    int n = slen[b];
+    int64_t s0 = sslot0[b];
+    if (n < 0 || n > max_len || s0 < 0 || s0 % TILE != 0 || s0 + n > slots) continue;
+    double ck[8], cv[8];
+    for (int m = 0; m < 8; ++m) {
+      ck[m] = lut_k[((size_t)l * H + h) * 8 + m];
+      cv[m] = lut_v[((size_t)l * H + h) * 8 + m];
+    }
+    double ebar_k = ebar ? ebar[((size_t)l * H + h) * 2] : 0.0;
+    double ebar_v = ebar ? ebar[((size_t)l * H + h) * 2 + 1] : 0.0;
+    int64_t region = ((int64_t)l * H + h) * slots;
+    for (int j = 0; j < n; ++j) {
+      int64_t s = s0 + j;
+      uint8_t kn[D], vn[D];
+      orc_unpack_slot(kc + region * 32, s, kn);
+      orc_unpack_slot_v(vc + region * 32, s, vn);
+      const uint16_t* scs = sc + (region + s) * 4;
+      double* ko = k_out + ((size_t)t * max_len + j) * D;
+      double* vo = v_out + ((size_t)t * max_len + j) * D;
+      dequant_k(kn, orc_f16_to_f32(scs[0]), orc_f16_to_f32(scs[1]), ck, flags, ebar_k, S, ko);
+      dequant_v(vn, orc_f16_to_f32(scs[2]), orc_f16_to_f32(scs[3]), cv, flags, ebar_v, S, vo);
+    }
   }
 }
