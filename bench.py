@@ -249,6 +249,13 @@ def main():
                "rotation_tflops": round(2 * 2 * 64 * 64 * pf_th / (pf_ms * 1e-3) / 1e12, 2)}
     del pf_cache, k_pf, v_pf
 
+    two_step = None
+    if not args.decode_only and not args.no_fp16_baseline:
+        attend(0)                                   # reps[0]["out"]: the fused output on replica 0
+        torch.cuda.synchronize()
+        two_step = two_step_baseline(torch, tq, params, reps, L, H, n_ctx, cs.view(-1, 32, 2),
+                                     [d["pi"].view(L, H, 64, 64) for d in reps], lut_d, S_d, K, attend_ms)
+
     fp16_base = None if args.decode_only or args.no_fp16_baseline else fp16_attention_baseline(
         torch, L * H, n_ctx, args.replica_bytes, K)
     if fp16_base:
@@ -289,6 +296,7 @@ def main():
                      "alg_bytes_per_launch": int(alg_bytes)},
         "cpu_baseline": cpu,
         "prefill_quantize": prefill,
+        "two_step_baseline": two_step,
         "fp16_attention_baseline": fp16_base,
         "paper_context": {"memory_reduction": "7.1x (Table 4, fp32 baseline, 'CUDA')",
                           "kv_fetch_speedup": "1.96x Triton vs PyTorch fetch_unpacked, 143 tokens, "
@@ -339,6 +347,65 @@ def fp16_attention_baseline(torch, units, n_ctx, replica_bytes, K):
     del kv
     torch.cuda.empty_cache()
     return out
+
+
+def two_step_baseline(torch, tq, params, reps, L, H, n_ctx, cs, pi_list, lut_d, S_d, K, fused_ms):
+    """The dequantize-then-attend path on the same packed caches (the analog of
+    the paper's Table 6 comparison, fused kernel against unpacking first):
+    tq_dequantize writes fp16 k~ and v~ rows of every cached token to HBM,
+    then PyTorch rotates the query (RoPE, Pi q'), runs
+    scaled_dot_product_attention over the rows and applies Pi^T. Context for
+    the fused kernel, not part of the path."""
+    import torch.nn.functional as F
+    dev = torch.device("cuda:0")
+    units = L * H
+    shape = (L, 1, H, n_ctx, 64)
+    ko = torch.empty(shape, dtype=torch.float16, device=dev)
+    vo = torch.empty(shape, dtype=torch.float16, device=dev)
+    s0 = torch.zeros(1, dtype=torch.int64, device=dev)
+    sl = torch.tensor([n_ctx], dtype=torch.int32, device=dev)
+    c, s = cs[n_ctx - 1, :, 0], cs[n_ctx - 1, :, 1]
+    R = len(reps)
+
+    def dequant(r):
+        tq.dequantize(params, reps[r]["cache"], s0, sl, n_ctx, lut_d, lut_d, S_d, k_out=ko, v_out=vo)
+
+    def attend(r):
+        qf = reps[r]["q"].float()
+        x0, x1 = qf[..., 0::2], qf[..., 1::2]
+        qr = torch.stack((x0 * c - x1 * s, x0 * s + x1 * c), dim=-1).reshape(qf.shape)
+        pi = pi_list[r]
+        qh = torch.matmul(pi.unsqueeze(1), qr.unsqueeze(-1)).squeeze(-1)     # [L, 1, H, 64]
+        oh = F.scaled_dot_product_attention(qh.half().reshape(1, units, 1, 64), ko.view(1, units, n_ctx, 64),
+                                            vo.view(1, units, n_ctx, 64), scale=0.125)
+        return torch.matmul(oh.float().reshape(L, 1, H, 1, 64), pi.unsqueeze(1)).reshape(L, 1, H, 64)
+
+    def timed(fn):
+        for r in range(3):
+            fn(r % R)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for k in range(K):
+            fn(k % R)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+
+    dq_ms = timed(dequant)
+    total_ms = timed(lambda r: (dequant(r), attend(r)))
+    dequant(0)
+    out = attend(0)
+    torch.cuda.synchronize()
+    th = units * n_ctx
+    res = {"dequantize_ms": round(dq_ms, 5), "total_ms": round(total_ms, 5),
+           "dequantize_gbs": round(th * (72 + 256) / (dq_ms * 1e-3) / 1e9, 1),
+           "rows_bytes": th * 256,
+           "fused_decode_attend_speedup": round(total_ms / fused_ms, 2),
+           "max_abs_diff_vs_fused": round(float((out - reps[0]["out"].float()).abs().max()), 5)}
+    del ko, vo
+    torch.cuda.empty_cache()
+    return res
 
 
 def measured_traffic(workload):

@@ -235,6 +235,33 @@ TQ_API tq_status tq_decode_step(const tq_params* params, const tq_cache* cache,
                          void* out, void* workspace, size_t workspace_bytes,
                          void* stream);
 
+/* Dequantize the cache into plain fp16 key and value rows: the first step of
+ * a "dequantize first, then attend" path, the comparison the paper makes for
+ * its fused kernel (Sec. 5.4, Table 6: unpack to full precision, then
+ * attention). For every layer, sequence b and head, token j < seq_len[b]:
+ *   k~_j = (n_k,j/8) ( c_K[idx_j] + alpha g_k,j S^T (2 s_j - 1) )
+ *          (TQ_QJL_PAPER: ebar_K (2 s_j - 1) in place of alpha g_k,j S^T (2 s_j - 1))
+ *   v~_j = (n_v,j/8) ( c_V[idx^V_j] (+ the same residual estimate from the V
+ *          signs and g_v,j, or ebar_V, with TQ_V_QJL) )
+ * in the basis the cache holds (rotated; values unrotated without
+ * TQ_V_ROTATE), so that q^ . k~_j is the score of tq_decode_attend and its
+ * o^ is the softmax-weighted mean of the v~_j (before Pi^T).
+ *
+ *   seq_slot0, seq_len  device [B], as tq_decode_attend; a sequence whose
+ *           range is invalid (or seq_len > max_len) is skipped.
+ *   max_len host: the token stride of the outputs, >= every seq_len.
+ *   lut_k, lut_v, qjl_s, ebar  as tq_decode_attend (qjl_s may be NULL with
+ *           TQ_QJL_PAPER; ebar is needed only then).
+ *   k_out, v_out device fp16 [nlayers][B][H][max_len][64], 16-byte aligned;
+ *           rows j >= seq_len[b] are not written.
+ * params->rope_cs is not used.
+ */
+TQ_API tq_status tq_dequantize(const tq_params* params, const tq_cache* cache, int32_t B,
+                               int32_t layer0, int32_t nlayers, const int64_t* seq_slot0,
+                               const int32_t* seq_len, int32_t max_len,
+                               const float* lut_k, const float* lut_v, const float* qjl_s,
+                               const float* ebar, void* k_out, void* v_out, void* stream);
+
 /* Workspace bytes tq_decode_attend and tq_decode_step need for these sizes:
  * 0 unless sequences are split across blocks (few units, long max_len), and
  * 0 for empty or invalid sizes. */

@@ -6,7 +6,7 @@ path runs in the library's HIP kernels. If the library is not built, calls
 raise ``RuntimeError`` (there is no fallback path).
 
 Entry points (same names as the C ABI without the ``tq_`` prefix):
-    rope_table, quantize_pack, decode_attend, decode_step,
+    rope_table, quantize_pack, decode_attend, decode_step, dequantize,
     decode_workspace_bytes, calibrate_rotation, calibrate_lut, cache_bytes, last_error, version
 """
 from __future__ import annotations
@@ -18,7 +18,7 @@ from dataclasses import dataclass
 import torch
 
 __all__ = [
-    "Params", "Cache", "TQError", "rope_table", "quantize_pack", "decode_attend", "decode_step",
+    "Params", "Cache", "TQError", "rope_table", "quantize_pack", "decode_attend", "decode_step", "dequantize",
     "decode_workspace_bytes", "calibrate_rotation", "calibrate_lut", "cache_bytes", "last_error", "version",
     "V_ROTATE", "V_QJL", "QJL_PAPER", "ROPE_HALF", "INPUT_ROTATED", "OUT_FP32", "lib_path",
 ]
@@ -70,6 +70,8 @@ def _load():
     L.tq_decode_attend.restype = i32
     L.tq_decode_step.argtypes = [P, P, P, P, P, i32, i32, i32, P, P, P, i32, P, P, P, P, P, P, P, sz, P]
     L.tq_decode_step.restype = i32
+    L.tq_dequantize.argtypes = [P, P, i32, i32, i32, P, P, i32, P, P, P, P, P, P, P]
+    L.tq_dequantize.restype = i32
     L.tq_decode_workspace_bytes.argtypes = [P, i32, i32, i32]
     L.tq_decode_workspace_bytes.restype = sz
     L.tq_calibrate_rotation.argtypes = [P, i32, i32, P, P, P]
@@ -217,6 +219,40 @@ def decode_attend(params: Params, cache: Cache, q, q_pos, seq_slot0, seq_len, ma
                               _ptr(lut_v), _ptr(qjl_s), _ptr(ebar), _ptr(out), _ptr(workspace),
                               wsz, _stream(q.device)))
     return out
+
+
+def dequantize(params: Params, cache: Cache, seq_slot0, seq_len, max_len: int, lut_k, lut_v, qjl_s,
+               ebar=None, layer0: int = 0, nlayers: int | None = None, k_out=None, v_out=None):
+    """The dequantized fp16 key and value rows of every cached token,
+    [nlayers][B][H][max_len][64] each (rows past a sequence's length are not
+    written). Returns (k_out, v_out)."""
+    L = _load()
+    _dev(seq_slot0, "seq_slot0", torch.int64)
+    _dev(seq_len, "seq_len", torch.int32)
+    for name, t in (("lut_k", lut_k), ("lut_v", lut_v)):
+        _dev(t, name, torch.float32)
+    if qjl_s is not None:
+        _dev(qjl_s, "qjl_s", torch.float32)
+    if ebar is not None:
+        _dev(ebar, "ebar", torch.float32)
+    B = seq_len.numel()
+    nl = params.num_layers - layer0 if nlayers is None else nlayers
+    shape = (nl, B, params.num_heads, int(max_len), 64)
+    dev = seq_len.device
+    if k_out is None:
+        k_out = torch.empty(shape, dtype=torch.float16, device=dev)
+    if v_out is None:
+        v_out = torch.empty(shape, dtype=torch.float16, device=dev)
+    for name, t in (("k_out", k_out), ("v_out", v_out)):
+        _dev(t, name, torch.float16)
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} must be {list(shape)}")
+    p = params.c()
+    c = cache.c()
+    _check(L.tq_dequantize(ctypes.byref(p), ctypes.byref(c), B, layer0, nl, _ptr(seq_slot0), _ptr(seq_len),
+                           int(max_len), _ptr(lut_k), _ptr(lut_v), _ptr(qjl_s), _ptr(ebar), _ptr(k_out),
+                           _ptr(v_out), _stream(dev)))
+    return k_out, v_out
 
 
 def decode_step(params: Params, cache: Cache, q, k, v, pos, seq_slot0, seq_len, max_len: int,

@@ -223,6 +223,36 @@ tq_status tq_decode_step(const tq_params* params, const tq_cache* cache, const v
                        lut_k, lut_v, qjl_s, ebar, out, workspace, workspace_bytes, stream, true);
 }
 
+tq_status tq_dequantize(const tq_params* params, const tq_cache* cache, int32_t B, int32_t layer0,
+                        int32_t nlayers, const int64_t* seq_slot0, const int32_t* seq_len, int32_t max_len,
+                        const float* lut_k, const float* lut_v, const float* qjl_s, const float* ebar,
+                        void* k_out, void* v_out, void* stream) {
+  tq_status s = check_params(params, false);
+  if (s != TQ_OK) return s;
+  if ((s = check_cache(cache)) != TQ_OK) return s;
+  if (params->flags & TQ_INPUT_ROTATED) return fail(TQ_ERR_ARG, "TQ_INPUT_ROTATED applies to tq_quantize_pack only");
+  if (B < 0 || nlayers < 0 || max_len < 0) return fail(TQ_ERR_ARG, "B, nlayers and max_len must be >= 0");
+  if (layer0 < 0 || layer0 + nlayers > params->num_layers)
+    return fail(TQ_ERR_DIM, "layers [%d, %d) outside [0, %d)", layer0, layer0 + nlayers, params->num_layers);
+  if ((int64_t)B * nlayers == 0 || max_len == 0) return ok();
+  const bool paper = (params->flags & TQ_QJL_PAPER) != 0;
+  if (!seq_slot0 || !seq_len || !lut_k || !lut_v || !k_out || !v_out || (!paper && !qjl_s))
+    return fail(TQ_ERR_ARG, "a required pointer is NULL");
+  if (paper && !ebar) return fail(TQ_ERR_ARG, "TQ_QJL_PAPER needs ebar");
+  if (!aligned(k_out, 16) || !aligned(v_out, 16)) return fail(TQ_ERR_ALIGN, "k_out and v_out must be 16-byte aligned");
+  if ((int64_t)max_len > cache->slots) return fail(TQ_ERR_CAPACITY, "max_len exceeds the cache slots");
+  if ((int64_t)B * params->num_heads > 65535 || nlayers > 65535)
+    return fail(TQ_ERR_ARG, "B * num_heads and nlayers must be at most 65535");
+  tq::DequantArgs a{};
+  a.B = B; a.H = params->num_heads; a.layer0 = layer0; a.nlayers = nlayers; a.flags = params->flags;
+  a.seq_slot0 = seq_slot0; a.seq_len = seq_len; a.max_len = max_len;
+  a.lut_k = lut_k; a.lut_v = lut_v; a.qjl_s = qjl_s; a.ebar = ebar;
+  a.k_codes = (const uint8_t*)cache->k_codes; a.v_codes = (const uint8_t*)cache->v_codes;
+  a.scalars = (const uint16_t*)cache->scalars; a.slots = cache->slots;
+  a.k_out = k_out; a.v_out = v_out;
+  return hip_status(tq::launch_dequantize(a, (hipStream_t)stream), "tq_dequantize launch");
+}
+
 tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t ncal, float* pi_out,
                                 float* sing_out, void* stream) {
   if (nheads < 0 || ncal < 0) return fail(TQ_ERR_ARG, "nheads and ncal must be >= 0");

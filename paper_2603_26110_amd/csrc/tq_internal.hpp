@@ -66,11 +66,30 @@ struct DecodeArgs {
 
 constexpr int kPartialFloats = 2 * 64 + 4;   // m, l, pad, pad, o[64], s[64]
 
+struct DequantArgs {
+  int B, H, layer0, nlayers;
+  uint32_t flags;
+  const int64_t* seq_slot0;
+  const int32_t* seq_len;
+  int max_len;             // token stride of the outputs
+  const float* lut_k;
+  const float* lut_v;
+  const float* qjl_s;
+  const float* ebar;
+  const uint8_t* k_codes;
+  const uint8_t* v_codes;
+  const uint16_t* scalars;
+  int64_t slots;
+  void* k_out;             // fp16 [nlayers][B][H][max_len][64]
+  void* v_out;
+};
+
 // Launchers (return the HIP status of the launch).
 hipError_t launch_rope_table(float* cs, int positions, double base, hipStream_t st);
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t st);
 void decode_plan(int units, int max_len, int* waves, int* nsplit, int* split_tiles);
 hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st);
+hipError_t launch_dequantize(const DequantArgs& a, hipStream_t st);
 // Initial levels of the table calibration (by value: a host array).
 struct LutInit {
   float c[8];

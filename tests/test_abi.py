@@ -38,7 +38,7 @@ def _defines():
 def test_header_declares_the_entry_points():
     assert _declared_functions() == sorted([
         "tq_cache_bytes", "tq_rope_table", "tq_quantize_pack", "tq_decode_attend", "tq_decode_step",
-        "tq_decode_workspace_bytes", "tq_calibrate_rotation", "tq_calibrate_lut", "tq_last_error",
+        "tq_dequantize", "tq_decode_workspace_bytes", "tq_calibrate_rotation", "tq_calibrate_lut", "tq_last_error",
         "tq_version"])
 
 
@@ -233,3 +233,26 @@ def test_calibrate_lut_argument_checks():
     assert c(good, ncal=0) == -1
     assert c(good, x=0) == -1
     assert c(good, nh=0) == 0 and tq.last_error() == ""
+
+
+def _dequant(p, c, B=1, max_len=64, ptrs=FAKE, out=FAKE, S=FAKE, ebar=None, layer0=0, nlayers=1):
+    L = tq._load()
+    P = ctypes.c_void_p
+    return L.tq_dequantize(ctypes.byref(p) if p is not None else None, ctypes.byref(c) if c is not None else None,
+                           B, layer0, nlayers, P(ptrs), P(ptrs), max_len, P(ptrs), P(ptrs),
+                           P(S) if S else None, P(ebar) if ebar else None, P(out), P(out), None)
+
+
+def test_dequantize_argument_checks():
+    assert _dequant(None, _cache()) == -1 and "params" in tq.last_error()
+    assert _dequant(_params(flags=1 | 16), _cache()) == -1 and "TQ_INPUT_ROTATED" in tq.last_error()
+    assert _dequant(_params(flags=1 | 4), _cache()) == -1 and "ebar" in tq.last_error()
+    assert _dequant(_params(), _cache(), S=0) == -1                     # the projected form needs S
+    assert _dequant(_params(), _cache(), layer0=2) == -2
+    assert _dequant(_params(), _cache(), max_len=129) == -5
+    assert _dequant(_params(), _cache(), out=FAKE + 2) == -3
+    assert _dequant(_params(), _cache(), ptrs=0) == -1
+    # nothing to do is success, with nothing launched
+    assert _dequant(_params(), _cache(), B=0) == 0
+    assert _dequant(_params(), _cache(), max_len=0) == 0
+    assert tq.last_error() == ""
