@@ -71,7 +71,8 @@ __device__ __forceinline__ int64_t tile_half_offset(int64_t tile, int c, int r) 
 //   xh[64]   rotated vector (overwritten by the residual r)
 //   L        ascending table and its midpoints (0.5f * (c_m + c_{m+1}))
 //   S        64 x 64 projection in LDS (row-major); unused unless sign_mode == 1
-//   sign_mode 0 none, 1 projected (S r), 2 per element (r)
+//   sign_mode 0 none, 1 projected (S r), 2 per element (r), 3 projected with
+//            the signs set by the caller (g is computed and stored, no bits)
 //   words[8] out: with KEY_WORDS the key word format (index of dimension 8w+j
 //            in bits 3j..3j+2, its sign in bit 24+j), else nibble words
 //            (idx | sign << 3 in bits 4j..4j+3)
@@ -126,6 +127,7 @@ __device__ __forceinline__ float nearest_level(float u, const Levels& L, float c
 
 struct QuantOut {
   uint32_t n16, g16;
+  float g;                 // ||r|| in binary32 (before the fp16 store)
 };
 
 template <bool KEY_WORDS>
@@ -177,6 +179,7 @@ __device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Level
   QuantOut o;
   o.n16 = store_norm(n);
   o.g16 = (sign_mode == 0) ? 0u : store_norm(g);
+  o.g = g;
   return o;
 }
 

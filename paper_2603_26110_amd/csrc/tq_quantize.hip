@@ -170,6 +170,104 @@ __device__ __forceinline__ void rotate_tokens(float (&out)[kDim], const QuantArg
     }
 }
 
+// Projected QJL sign bits of the wave's 64 residuals (lane l: r of token
+// j0 + l, in registers): bit i = !(p_i < 0) for p_i = the binary32 fma chain
+// over k ascending of S[i][k] r_k (the exact quantizer step). p is first
+// computed on the matrix cores as D = S R^T (fp32 products and sums, another
+// order); a 64-term fp32 dot product in any order is within 2^-17 sum_k
+// |S_ik r_k| <= 2^-17 ||S_i|| ||r|| of the exact value, so where
+// |p~_i| > 2^-14 ||S_i|| ||r|| its sign is the chain's, and only the
+// coordinates inside that band are recomputed with the chain.
+// The residuals reach the instruction's B layout through the same
+// v_permlane32_swap pairs that handed the rotated values to the lanes (a swap
+// undoes itself), and go back the same way.
+__device__ __forceinline__ uint64_t projected_signs(float (&x)[kDim], float g, const float* s_S,
+                                                    const float* s_Sn, int lane) {
+  const int n = lane & 31, hh = lane >> 5;
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int d = 32 * mb + 8 * (r >> 2) + (r & 3);
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[d]), __float_as_uint(x[d + 4]), false,
+                                                       false);
+      x[d] = __uint_as_float(sw[0]);       // token n, dimension d + 4h
+      x[d + 4] = __uint_as_float(sw[1]);   // token 32 + n, dimension d + 4h
+    }
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) { acc[0][0][r] = 0.0f; acc[1][0][r] = 0.0f; acc[0][1][r] = 0.0f; acc[1][1][r] = 0.0f; }
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    int o = n * kPiPitch + 8 * q + 4 * hh;
+    asm volatile("" : "+v"(o));
+    const float4 p0 = *reinterpret_cast<const float4*>(s_S + o);
+    const float4 p1 = *reinterpret_cast<const float4*>(s_S + o + 32 * kPiPitch);
+    const float a0[4] = {p0.x, p0.y, p0.z, p0.w}, a1[4] = {p1.x, p1.y, p1.z, p1.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[j], x[8 * q + j], acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[j], x[8 * q + 4 + j], acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[j], x[8 * q + j], acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[j], x[8 * q + 4 + j], acc[1][1], 0, 0, 0);
+    }
+  }
+  // residuals back to one token per lane; p~ likewise
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int d = 32 * mb + 8 * (r >> 2) + (r & 3);
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[d]), __float_as_uint(x[d + 4]), false,
+                                                       false);
+      x[d] = __uint_as_float(sw[0]);
+      x[d + 4] = __uint_as_float(sw[1]);
+      const auto sp = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[mb][0][r]),
+                                                       __float_as_uint(acc[mb][1][r]), false, false);
+      acc[mb][0][r] = __uint_as_float(sp[0]);   // p~ of row d
+      acc[mb][1][r] = __uint_as_float(sp[1]);   // p~ of row d + 4
+    }
+  uint64_t bits = 0, flagged = 0;
+  const float gb = g * 0x1p-14f;
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int i = 32 * mb + 8 * (r >> 2) + (r & 3) + 4 * half;
+        const float pv = acc[mb][half][r];
+        const bool sure = fabsf(pv) > s_Sn[i] * gb;
+        bits |= (uint64_t)((sure && !(pv < 0.0f)) ? 1u : 0u) << i;
+        flagged |= (uint64_t)(sure ? 0u : 1u) << i;
+      }
+  // rows inside the band, any lane: the fixed-order chain (wave-uniform row)
+  uint64_t any = flagged;
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) {
+    const uint32_t lo = __shfl_xor((uint32_t)any, o, 64), hi = __shfl_xor((uint32_t)(any >> 32), o, 64);
+    any |= ((uint64_t)hi << 32) | lo;
+  }
+  while (any) {
+    const int i = __builtin_ctzll(any);
+    any &= any - 1;
+    if ((flagged >> i) & 1ull) {
+      const float4* row = reinterpret_cast<const float4*>(s_S + i * kPiPitch);
+      float acc_i = 0.0f;
+#pragma unroll
+      for (int k4 = 0; k4 < kDim / 4; ++k4) {
+        const float4 sv = row[k4];
+        acc_i = fmaf(sv.x, x[4 * k4 + 0], acc_i);
+        acc_i = fmaf(sv.y, x[4 * k4 + 1], acc_i);
+        acc_i = fmaf(sv.z, x[4 * k4 + 2], acc_i);
+        acc_i = fmaf(sv.w, x[4 * k4 + 3], acc_i);
+      }
+      bits |= (uint64_t)((acc_i < 0.0f) ? 0u : 1u) << i;
+    }
+  }
+  return bits;
+}
+
 // ----------------------------------------------------- lane-per-token kernel
 // Block: 4 waves x 64 tokens of one (layer, sequence, head). Grid:
 // x = ceil(T/256), y = B*H, z = nlayers. LDS: Pi (pitch 68) for the
@@ -178,7 +276,8 @@ __device__ __forceinline__ void rotate_tokens(float (&out)[kDim], const QuantArg
 template <bool F16, bool VQJL>
 __global__ __launch_bounds__(256) void quantize_tiles_kernel(QuantArgs a) {
   __shared__ __attribute__((aligned(16))) float s_pi[kDim * kPiPitch];
-  __shared__ __attribute__((aligned(16))) float s_S[kDim * kDim];
+  __shared__ __attribute__((aligned(16))) float s_S[kDim * kPiPitch];
+  __shared__ float s_Sn[kDim];                                       // ||S_i|| (fp32)
   __shared__ uint32_t s_vt[4][kDim * 8];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
@@ -187,13 +286,19 @@ __global__ __launch_bounds__(256) void quantize_tiles_kernel(QuantArgs a) {
   const int64_t lh = (int64_t)l * a.H + h;
   const bool rotated = (a.flags & kInputRotated) != 0;
   const bool paper = (a.flags & kQjlPaper) != 0;
-  const int ksign = paper ? 2 : 1;
-  const int vsign = VQJL ? ksign : 0;   // (a V sign pass is compiled only where asked for)
+  const int vsign = VQJL ? (paper ? 2 : 1) : 0;   // (a V sign pass is compiled only where asked for)
 
   for (int e = threadIdx.x; e < kDim * kDim / 4; e += blockDim.x) {
     const float4 pv = reinterpret_cast<const float4*>(a.pi + lh * kDim * kDim)[e];
     *reinterpret_cast<float4*>(s_pi + (e >> 4) * kPiPitch + (e & 15) * 4) = pv;
-    reinterpret_cast<float4*>(s_S)[e] = reinterpret_cast<const float4*>(a.qjl_s)[e];
+    *reinterpret_cast<float4*>(s_S + (e >> 4) * kPiPitch + (e & 15) * 4) =
+        reinterpret_cast<const float4*>(a.qjl_s)[e];
+  }
+  if (threadIdx.x < kDim) {
+    const float* srow = a.qjl_s + threadIdx.x * kDim;
+    float ss = 0.0f;
+    for (int k = 0; k < kDim; ++k) ss = fmaf(srow[k], srow[k], ss);
+    s_Sn[threadIdx.x] = sqrtf(ss);
   }
   const Levels Lk = load_levels(a.lut_k + lh * 8);
   const Levels Lv = load_levels(a.lut_v + lh * 8);
@@ -222,7 +327,12 @@ __global__ __launch_bounds__(256) void quantize_tiles_kernel(QuantArgs a) {
     rotate_tokens<F16>(x, a, a.k, s_pi, li, b, h, j0, lane, true);
   }
   uint32_t kw[8];
-  const QuantOut qk = quantize_lane<true>(x, Lk, s_S, ksign, kw);
+  const QuantOut qk = quantize_lane<true>(x, Lk, s_S, paper ? 2 : 3, kw);
+  if (!paper) {
+    const uint64_t sb = projected_signs(x, qk.g, s_S, s_Sn, lane);
+#pragma unroll
+    for (int w = 0; w < 8; ++w) kw[w] |= (uint32_t)((sb >> (8 * w)) & 0xFFu) << 24;
+  }
   if (ok) {
     const int64_t tile = slot >> 6;
     const int r = (int)(slot & 63);
@@ -240,7 +350,12 @@ __global__ __launch_bounds__(256) void quantize_tiles_kernel(QuantArgs a) {
     for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.v, row + i, F16) : 0.0f;
   }
   uint32_t vw[8];
-  const QuantOut qv = quantize_lane<false>(x, Lv, s_S, vsign, vw);
+  const QuantOut qv = quantize_lane<false>(x, Lv, s_S, (VQJL && !paper) ? 3 : vsign, vw);
+  if (VQJL && !paper) {
+    const uint64_t sb = projected_signs(x, qv.g, s_S, s_Sn, lane);
+#pragma unroll
+    for (int i = 0; i < kDim; ++i) vw[i >> 3] |= (uint32_t)((sb >> i) & 1ull) << (4 * (i & 7) + 3);
+  }
   if (ok) {
     *reinterpret_cast<uint2*>(a.scalars + (lh * a.slots + slot) * 4) =
         make_uint2(qk.n16 | (qk.g16 << 16), qv.n16 | (qv.g16 << 16));
