@@ -21,7 +21,7 @@ import pytest
 import torch
 
 import paper_2603_26110_amd as tq
-from gpu_cases import GAUSS_LUT, fp16_ulp
+from gpu_cases import DeviceBytes, GAUSS_LUT, fp16_ulp, unpack_slot
 from oracle import oracle
 from paper_2603_26110_amd import synth
 
@@ -41,16 +41,14 @@ def _i64(x):
 
 def _gpu_region(cache, l, h, s0, n):
     """The GPU's bytes of slots [s0, s0 + cap) of one (layer, head) region as
-    a one-head oracle.Cache layout, cap = n rounded up to a tile (s0 is
-    tile-aligned, so tile layouts are unchanged by the shift). Compared with
-    the oracle's bytes, never given to the oracle."""
+    a one-head layout, cap = n rounded up to a tile (s0 is tile-aligned, so
+    tile layouts are unchanged by the shift). Compared with the oracle's
+    bytes, never given to the oracle."""
     cap = (n + 63) // 64 * 64
-    oc = oracle.Cache(1, 1, cap)
     base = (l * cache.num_heads + h) * cache.slots + s0
-    oc.k[:] = cache.k_codes[base * 32:(base + cap) * 32].cpu().numpy()
-    oc.v[:] = cache.v_codes[base * 32:(base + cap) * 32].cpu().numpy()
-    oc.s[:] = cache.scalars[base * 4:(base + cap) * 4].cpu().numpy().view(np.uint16)
-    return oc
+    return DeviceBytes(1, 1, cap, cache.k_codes[base * 32:(base + cap) * 32].cpu().numpy(),
+                       cache.v_codes[base * 32:(base + cap) * 32].cpu().numpy(),
+                       cache.scalars[base * 4:(base + cap) * 4].cpu().numpy().view(np.uint16))
 
 
 def _oracle_unit_cache(krows, vrows, l, h, pi, lut_k, lut_v, S, flags, cs_host):
@@ -105,7 +103,7 @@ def _check_codes(cache, samples, cs_host, pi, lut_k, lut_v, S, flags):
             xh = oracle.rotated_input(np.asarray(x, np.float32), is_key, pos, cs_host, pi[l, h],
                                       rotate_v=bool(flags & tq.V_ROTATE))
             nib, n16, _ = oracle.quantize_vector(xh, lut[l, h], S, oracle.SIGN_PROJECTED if is_key else 0)
-            got = oracle.unpack_slot(oc.region(which, 0, 0), r, which)
+            got = unpack_slot(oc.region(which, 0, 0), r, which)
             bad = (got & 7) != (nib & 7)
             if bad.any():
                 xd = xh.astype(np.float64)

@@ -16,7 +16,8 @@ import pytest
 import torch
 
 import paper_2603_26110_amd as tq
-from gpu_cases import Case, GAUSS_LUT, fp16_ulp, to_gpu, to_oracle
+from gpu_cases import (Case, GAUSS_LUT, assert_agree_up_to_threshold_rounding, device_bytes, fp16_ulp,
+                       to_gpu)
 from oracle import oracle
 from paper_2603_26110_amd import synth
 
@@ -80,53 +81,11 @@ def test_quantize_bit_exact_on_rotated_inputs(T, B, slot0, flags):
     torch.cuda.synchronize()
     oc = oracle.Cache(L, H, 1152)
     case.oracle_quantize(oc, k=kh, v=vh)
-    got = to_oracle(cache)
+    got = device_bytes(cache)
     np.testing.assert_array_equal(got.s, oc.s)
     np.testing.assert_array_equal(got.k, oc.k)
     np.testing.assert_array_equal(got.v, oc.v)
     assert oc.s.any()
-
-
-def _threshold_distance(case, oc_flags, li, b, j, h, is_key):
-    x = (case.k if is_key else case.v)[li, b, j, h].astype(np.float32)
-    l = case.layer0 + li
-    xh = oracle.rotated_input(x, is_key, int(case.pos0[b]) + j, case.cs_host, case.pi[l, h],
-                              rotate_v=bool(oc_flags & tq.V_ROTATE))
-    xd = xh.astype(np.float64)
-    u = xd * 8.0 / np.linalg.norm(xd)
-    lut = (case.lut_k if is_key else case.lut_v)[l, h].astype(np.float64)
-    t = 0.5 * (lut[:-1] + lut[1:])
-    return np.min(np.abs(u[:, None] - t[None, :]), axis=1)
-
-
-def _assert_agree_up_to_threshold_rounding(case, got, ref, B, T, H):
-    """Two caches quantized from the same raw inputs by two binary32 paths
-    (RoPE and rotation summed in different orders): the fp16 norms agree to
-    one ulp and a code differs only where the exact coordinate sits within
-    rounding of a decision threshold, by one level."""
-    ng = got.s.view(np.float16).astype(np.float64)
-    no = ref.s.view(np.float16).astype(np.float64)
-    assert np.all(np.abs(ng - no) <= fp16_ulp(no) + 1e-12)
-    code_diff = sign_diff = total = 0
-    for b in range(B):
-        for j in range(T):
-            s = int(case.slot0[b]) + j
-            for h in range(H):
-                for is_key, which in ((True, "k"), (False, "v")):
-                    ng_ = oracle.unpack_slot(got.region(which, 0, h), s, which)
-                    no_ = oracle.unpack_slot(ref.region(which, 0, h), s, which)
-                    total += 64
-                    bad = (ng_ & 7) != (no_ & 7)
-                    sign_diff += int(((ng_ >> 3) != (no_ >> 3)).sum())
-                    if bad.any():
-                        code_diff += int(bad.sum())
-                        dist = _threshold_distance(case, case.flags, 0, b, j, h, is_key)
-                        assert np.all(dist[bad] < 1e-4), (b, j, h, which, dist[bad])
-                        assert np.all(np.abs((ng_[bad] & 7).astype(int) - (no_[bad] & 7)) == 1)
-    assert code_diff <= 1e-3 * total
-    # a sign bit follows the residual: it may flip with a code, or where its
-    # projection is within rounding of zero
-    assert sign_diff <= 64 * code_diff + 1e-4 * total
 
 
 def test_quantize_kernels_agree_on_raw_inputs():
@@ -143,7 +102,7 @@ def test_quantize_kernels_agree_on_raw_inputs():
         case.gpu_quantize(b, k=case.t("k")[:, :, sl].contiguous(), v=case.t("v")[:, :, sl].contiguous(),
                           pos0=[j0], slot0=[j0])
     torch.cuda.synchronize()
-    _assert_agree_up_to_threshold_rounding(case, to_oracle(a), to_oracle(b), 1, T, H)
+    assert_agree_up_to_threshold_rounding(case, device_bytes(a), device_bytes(b), 1, T, H)
 
 
 @pytest.mark.parametrize("T", [256, 3])
@@ -155,7 +114,7 @@ def test_quantize_end_to_end_matches_up_to_threshold_rounding(T):
     torch.cuda.synchronize()
     oc = oracle.Cache(L, H, case.slots)
     case.oracle_quantize(oc)
-    _assert_agree_up_to_threshold_rounding(case, to_oracle(cache), oc, B, T, H)
+    assert_agree_up_to_threshold_rounding(case, device_bytes(cache), oc, B, T, H)
 
 
 # --------------------------------------------------------------------- decode
