@@ -88,6 +88,39 @@ def test_quantize_bit_exact_on_rotated_inputs(T, B, slot0, flags):
     assert oc.s.any()
 
 
+@pytest.mark.parametrize("flags", [tq.V_ROTATE, tq.V_ROTATE | tq.V_QJL])
+def test_projected_signs_inside_the_guard_band_are_exact(flags):
+    # The tile kernel takes a projected sign from its matrix-core product only
+    # where |p_i| > 2^-14 ||S_i|| ||r|| and runs the fixed-order chain
+    # elsewhere. Rows of S built to land in that band: a zero row (p = 0,
+    # sign +1), a row of tiny entries, rows with one nonzero entry (exact
+    # products), and a row that cancels to a few ulps for most residuals.
+    L, H, B, T = 2, 3, 1, 256
+    flags |= tq.INPUT_ROTATED
+    case = Case(14, L, H, B, T, io="f32", flags=flags, slots=256, slot0=[0], layer0=1, nl=1)
+    g = synth.rng(15)
+    S = g.standard_normal((64, 64)).astype(np.float32)
+    S[0] = 0.0
+    S[1] *= np.float32(2.0 ** -60)
+    S[2] = 0.0
+    S[2, 5] = 1.0
+    S[3] = 0.0
+    S[3, 9] = -3.0
+    S[4] = np.float32(1.0) + (np.arange(64) % 2).astype(np.float32) * np.float32(2.0 ** -22)
+    S[4, 32:] *= -1.0
+    case.S = S
+    kh, vh = _rotated_inputs(41, 1, B, T, H)
+    cache = tq.Cache(L, H, 256)
+    case.gpu_quantize(cache, k=torch.from_numpy(kh).cuda(), v=torch.from_numpy(vh).cuda())
+    torch.cuda.synchronize()
+    oc = oracle.Cache(L, H, 256)
+    case.oracle_quantize(oc, k=kh, v=vh)
+    got = device_bytes(cache)
+    np.testing.assert_array_equal(got.s, oc.s)
+    np.testing.assert_array_equal(got.k, oc.k)
+    np.testing.assert_array_equal(got.v, oc.v)
+
+
 def test_quantize_kernels_agree_on_raw_inputs():
     # The tile kernel (T >= 64, rotations on the matrix cores) and the wave
     # kernel (T < 64, fma chains) sum the rotations in different orders: the
