@@ -166,7 +166,7 @@ def threshold_distance(case, oc_flags, li, b, j, h, is_key):
     x = (case.k if is_key else case.v)[li, b, j, h].astype(np.float32)
     l = case.layer0 + li
     xh = oracle.rotated_input(x, is_key, int(case.pos0[b]) + j, case.cs_host, case.pi[l, h],
-                              rotate_v=bool(oc_flags & tq.V_ROTATE))
+                              half=bool(oc_flags & tq.ROPE_HALF), rotate_v=bool(oc_flags & tq.V_ROTATE))
     xd = xh.astype(np.float64)
     u = xd * 8.0 / np.linalg.norm(xd)
     lut = (case.lut_k if is_key else case.lut_v)[l, h].astype(np.float64)

@@ -138,10 +138,11 @@ def test_quantize_kernels_agree_on_raw_inputs():
     assert_agree_up_to_threshold_rounding(case, device_bytes(a), device_bytes(b), 1, T, H)
 
 
+@pytest.mark.parametrize("flags", [tq.V_ROTATE, tq.V_ROTATE | tq.ROPE_HALF, 0, tq.V_ROTATE | tq.V_QJL])
 @pytest.mark.parametrize("T", [256, 3])
-def test_quantize_end_to_end_matches_up_to_threshold_rounding(T):
+def test_quantize_end_to_end_matches_up_to_threshold_rounding(T, flags):
     L, H, B = 1, 8, 2
-    case = Case(13, L, H, B, T, io="f16", slots=2 * 320, slot0=[0, 320], pos0=[0, 17])
+    case = Case(13, L, H, B, T, io="f16", flags=flags, slots=2 * 320, slot0=[0, 320], pos0=[0, 17])
     cache = tq.Cache(L, H, case.slots)
     case.gpu_quantize(cache)
     torch.cuda.synchronize()
