@@ -244,7 +244,7 @@ def main():
     pf_th = L * H * T
     pf_bytes = pf_th * (2 * 64 * io_b + 72)
     prefill = {"ms": round(pf_ms, 4), "token_heads": pf_th,
-               "kernel": "quantize_tiles_kernel (rotations and S r on fp32 MFMA, quantizer steps on VALU)",
+               "kernel": "quantize_tiles_kernel (rotations and S r on fp16 MFMA with hi/lo parts, quantizer steps on VALU)",
                "alg_bytes": pf_bytes, "gbs": round(pf_bytes / (pf_ms * 1e-3) / 1e9, 1),
                "rotation_tflops": round(2 * 2 * 64 * 64 * pf_th / (pf_ms * 1e-3) / 1e12, 2)}
     del pf_cache, k_pf, v_pf

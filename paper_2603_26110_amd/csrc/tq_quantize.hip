@@ -5,8 +5,9 @@
 // Two kernels:
 //   quantize_tiles_kernel   for prefill-sized T: 64 tokens per wave; the
 //                           rotations x^ = Pi x' of the wave's 64 x 64 block
-//                           run on the matrix cores (fp32 MFMA), then one lane
-//                           per token runs the quantizer steps.
+//                           and the projections S r run on the matrix cores
+//                           (fp16 MFMA on hi/lo parts), one lane per token
+//                           runs the quantizer steps.
 //   quantize_vectors_kernel one wave per vector (one lane per dimension; the
 //                           key and the value of a token-head in parallel), for
 //                           decode-step appends with small T; its rotation is
@@ -41,123 +42,82 @@ hipError_t launch_rope_table(float* cs, int positions, double base, hipStream_t 
   return hipGetLastError();
 }
 
-// ------------------------------------------------- MFMA rotation of 64 rows
-// x^ = Pi x' for the 64 tokens of a wave as D = Pi X'^T on the matrix cores
-// (v_mfma_f32_32x32x2f32: fp32 products, fp32 sums), in two 32-row blocks of
-// Pi (mb) times two 32-token blocks (nb), 32 rank-2 steps each.
-// Operand layout of the instruction (lane l, n = l % 32, h = l / 32):
-//   A lane value  A[n][h]       (row n of the 32 x 2 slice)
-//   B lane value  B[h][n]       (column n of the 2 x 32 slice)
-//   D register r  D[8 (r/4) + 4h + r%4][n]
-// Step s (q = s/4, jj = s%4) gives lane half h the contraction index
-// k = 8q + 4h + jj, so the 32 k a lane contributes are the dimensions
-// {8q + 4h + jj}: the same set that D leaves in that lane half. A lane's
-// B values are therefore 8 groups of 4 consecutive dimensions of its token
-// (one 8- or 16-byte load each) and its A values are 4 consecutive columns
-// of a row of Pi (one 16-byte LDS read per q).
+// ------------------------------------------- matrix-core products of 64 rows
+// Two dense 64 x 64 x 64 products per wave run on the matrix cores: the
+// rotation x^ = Pi x' of the wave's 64 tokens and the QJL projection S r of
+// their residuals. Both use v_mfma_f32_32x32x16_f16 (fp16 inputs, fp32 sums)
+// with each fp32 operand split into fp16 parts hi = fp16(v), lo = fp16(v - hi)
+// and three products hi*hi + hi*lo + lo*hi, which carries a product to about
+// 2^-21 relative. Each token's vector is first scaled by a power of two
+// (exact) so that its largest entry lies in [1, 2), and each row of S
+// likewise, which keeps the parts in fp16's range; the results are scaled
+// back (exact) or compared with equally scaled bounds.
+// Instruction layout (lane l, n = l % 32, h = l / 32; verified on gfx950):
+//   A lane values A[n][8h + j], B lane values B[8h + j][n] (j = 0..7),
+//   D register r D[8 (r/4) + 4h + r%4][n].
+// Step q (0..3) contracts k = 16q + 8h + j: a lane's B values at step q are 8
+// consecutive dimensions of its token (one 16-byte load of fp16 input) and
+// its A values 8 consecutive columns of a row of the staged matrix (one
+// 16-byte LDS read per part). The result leaves lane half h the dimensions
+// {8q + 4h + j, j < 4} of its two tokens (32 nb + n, nb = 0, 1); one
+// v_permlane32_swap per register pair then hands lane l all 64 values of
+// token l.
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 
-// Pitch of the staged Pi: 16-byte row reads of 16 lanes (rows n, 4n dwords
-// apart modulo 64 banks) are conflict-free.
-constexpr int kPiPitch = 68;
+// Halfs per staged row: the 16-byte reads of 16 rows (36 dwords apart) fall
+// on all 64 banks once.
+constexpr int kHPitch = 72;
 
-// Loads the lane's half row of token j0 + 32 nb + n (values x'[8q + 4h + jj]
-// at step 4q + jj) and applies RoPE (keys): both pairings keep a pair inside
-// the lane's set (interleaved: (2m, 2m + 1) inside one group of 4; half: d and
-// d + 32 in groups q and q + 4).
-template <bool F16>
-__device__ __forceinline__ void load_half_row(float (&xv)[32], const QuantArgs& a, const void* src, int li,
-                                              int b, int h, int j0, int nb, int lane, bool rope) {
-  const int n = lane & 31, hh = lane >> 5;
-  const bool half = (a.flags & kRopeHalf) != 0;
-  const int j = j0 + 32 * nb + n;
-  const int pos = a.pos0[b] + j;
-  const bool ok = j < a.T && (!rope || (pos >= 0 && pos < a.rope_positions));
-  const int64_t row = ((((int64_t)li * a.B + b) * a.T + j) * a.H + h) * kDim;
+struct SplitOps {
+  half8 hi[2][4], lo[2][4];   // [token block nb][step q]
+};
+
+__device__ __forceinline__ void split8(const float* v, float sc, half8& hi, half8& lo) {
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int d0 = 8 * q + 4 * hh;
-    float4 f = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (ok) {
-      if (F16) {
-        const uint2 w = *reinterpret_cast<const uint2*>(reinterpret_cast<const __half*>(src) + row + d0);
-        f.x = half_bits_to_float(w.x); f.y = half_bits_to_float(w.x >> 16);
-        f.z = half_bits_to_float(w.y); f.w = half_bits_to_float(w.y >> 16);
-      } else {
-        f = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(src) + row + d0);
-      }
-    }
-    xv[4 * q + 0] = f.x; xv[4 * q + 1] = f.y; xv[4 * q + 2] = f.z; xv[4 * q + 3] = f.w;
-  }
-  if (!rope || !ok) return;
-  const float4* cs4 = reinterpret_cast<const float4*>(a.rope_cs + (int64_t)pos * 2 * kPairs);
-  if (!half) {
-    // pairs d0/2 and d0/2 + 1 of group q: their (cos, sin) in one float4
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const float4 c = cs4[2 * q + hh];
-      const float x0 = xv[4 * q], x1 = xv[4 * q + 1], x2 = xv[4 * q + 2], x3 = xv[4 * q + 3];
-      xv[4 * q + 0] = x0 * c.x - x1 * c.y; xv[4 * q + 1] = x0 * c.y + x1 * c.x;
-      xv[4 * q + 2] = x2 * c.z - x3 * c.w; xv[4 * q + 3] = x2 * c.w + x3 * c.z;
-    }
-  } else {
-    // pair (d, d + 32) for d in group q < 4, angle index d
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int d0 = 8 * q + 4 * hh;
-      const float4 c01 = cs4[d0 >> 1], c23 = cs4[(d0 >> 1) + 1];
-      const float cc[4] = {c01.x, c01.z, c23.x, c23.z}, ss[4] = {c01.y, c01.w, c23.y, c23.w};
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        const float xa = xv[4 * q + jj], xb = xv[4 * (q + 4) + jj];
-        xv[4 * q + jj] = xa * cc[jj] - xb * ss[jj];
-        xv[4 * (q + 4) + jj] = xa * ss[jj] + xb * cc[jj];
-      }
-    }
+  for (int j = 0; j < 8; ++j) {
+    const float x = v[j] * sc;
+    const _Float16 a = (_Float16)x;
+    hi[j] = a;
+    lo[j] = (_Float16)(x - (float)a);
   }
 }
 
-// acc[mb] += the 32 rank-2 steps of row block mb of Pi times one token block.
-// The Pi reads are issued per group q (the empty asm keeps the compiler from
-// holding all 64 values of Pi in registers across both token blocks).
-__device__ __forceinline__ void rotate_block(const float (&xv)[32], const float* s_pi, int lane,
-                                             f32x16& acc0, f32x16& acc1) {
-  const int n = lane & 31, hh = lane >> 5;
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    int o = n * kPiPitch + 8 * q + 4 * hh;
-    asm volatile("" : "+v"(o));
-    const float4 p0 = *reinterpret_cast<const float4*>(s_pi + o);
-    const float4 p1 = *reinterpret_cast<const float4*>(s_pi + o + 32 * kPiPitch);
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(p0.x, xv[4 * q + 0], acc0, 0, 0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(p1.x, xv[4 * q + 0], acc1, 0, 0, 0);
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(p0.y, xv[4 * q + 1], acc0, 0, 0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(p1.y, xv[4 * q + 1], acc1, 0, 0, 0);
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(p0.z, xv[4 * q + 2], acc0, 0, 0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(p1.z, xv[4 * q + 2], acc1, 0, 0, 0);
-    acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(p0.w, xv[4 * q + 3], acc0, 0, 0, 0);
-    acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(p1.w, xv[4 * q + 3], acc1, 0, 0, 0);
-  }
+// 2^(1 - e) for m = f 2^e, f in [0.5, 1): m times it lies in [1, 2); 1 for m = 0.
+__device__ __forceinline__ float unit_scale(float m) {
+  if (!(m > 0.0f)) return 1.0f;
+  int e;
+  frexpf(m, &e);
+  return ldexpf(1.0f, 1 - e);
 }
 
-// Rotates the wave's 64 tokens and hands lane l all 64 rotated values of token
-// j0 + l: after the products, lane half h of token block nb holds dimensions
-// {8q + 4h + jj} of token 32 nb + n; one v_permlane32_swap per register pair
-// moves the upper half of block 0 and the lower half of block 1 across, so
-// that lane l < 32 holds token l and lane l >= 32 token l (32 + n).
-template <bool F16>
-__device__ __forceinline__ void rotate_tokens(float (&out)[kDim], const QuantArgs& a, const void* src,
-                                              const float* s_pi, int li, int b, int h, int j0, int lane,
-                                              bool rope) {
-  f32x16 acc[2][2];
+// acc[mb][nb] = rows 32 mb .. 32 mb + 31 of the staged matrix times the
+// wave's token blocks, as hi*hi + hi*lo + lo*hi.
+__device__ __forceinline__ void split_products(const SplitOps& b, const _Float16* mh, const _Float16* ml,
+                                               int lane, f32x16 (&acc)[2][2]) {
+  const int n = lane & 31, hh = lane >> 5;
 #pragma unroll
   for (int r = 0; r < 16; ++r) { acc[0][0][r] = 0.0f; acc[1][0][r] = 0.0f; acc[0][1][r] = 0.0f; acc[1][1][r] = 0.0f; }
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) {
-    float xv[32];
-    load_half_row<F16>(xv, a, src, li, b, h, j0, nb, lane, rope);
-    rotate_block(xv, s_pi, lane, acc[0][nb], acc[1][nb]);
+  for (int q = 0; q < 4; ++q) {
+    int o = n * kHPitch + 16 * q + 8 * hh;
+    asm volatile("" : "+v"(o));
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb) {
+      const half8 ah = *reinterpret_cast<const half8*>(mh + o + 32 * mb * kHPitch);
+      const half8 al = *reinterpret_cast<const half8*>(ml + o + 32 * mb * kHPitch);
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, b.hi[nb][q], acc[mb][nb], 0, 0, 0);
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, b.lo[nb][q], acc[mb][nb], 0, 0, 0);
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(al, b.hi[nb][q], acc[mb][nb], 0, 0, 0);
+      }
+    }
   }
+}
+
+// D blocks -> lane l holds all 64 rows for token l (column l of the block pair).
+__device__ __forceinline__ void to_lane_per_token(f32x16 (&acc)[2][2], float (&out)[kDim]) {
 #pragma unroll
   for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -165,82 +125,163 @@ __device__ __forceinline__ void rotate_tokens(float (&out)[kDim], const QuantArg
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[mb][0][r]),
                                                        __float_as_uint(acc[mb][1][r]), false, false);
       const int d = 32 * mb + 8 * (r >> 2) + (r & 3);
-      out[d] = __uint_as_float(sw[0]);       // dimension set of lane half 0
-      out[d + 4] = __uint_as_float(sw[1]);   // dimension set of lane half 1
+      out[d] = __uint_as_float(sw[0]);       // row set of lane half 0
+      out[d + 4] = __uint_as_float(sw[1]);   // row set of lane half 1
     }
 }
 
-// Projected QJL sign bits of the wave's 64 residuals (lane l: r of token
-// j0 + l, in registers): bit i = !(p_i < 0) for p_i = the binary32 fma chain
-// over k ascending of S[i][k] r_k (the exact quantizer step). p is first
-// computed on the matrix cores as D = S R^T (fp32 products and sums, another
-// order); a 64-term fp32 dot product in any order is within 2^-17 sum_k
-// |S_ik r_k| <= 2^-17 ||S_i|| ||r|| of the exact value, so where
-// |p~_i| > 2^-14 ||S_i|| ||r|| its sign is the chain's, and only the
-// coordinates inside that band are recomputed with the chain.
-// The residuals reach the instruction's B layout through the same
-// v_permlane32_swap pairs that handed the rotated values to the lanes (a swap
-// undoes itself), and go back the same way.
-__device__ __forceinline__ uint64_t projected_signs(float (&x)[kDim], float g, const float* s_S,
-                                                    const float* s_Sn, int lane) {
+// Loads the lane's values x'[16q + 8h + j] of tokens j0 + n (nb = 0) and
+// j0 + 32 + n (nb = 1), applies RoPE (keys; both pairings keep a pair inside
+// the lane: (2m, 2m + 1) inside a group of 8, (d, d + 32) in groups q and
+// q + 2), scales each token by a power of two and splits it. Returns the
+// lane's token scale (of token j0 + lane, for scaling the result back).
+template <bool F16>
+__device__ __forceinline__ float load_split_rows(SplitOps& ops, const QuantArgs& a, const void* src, int li,
+                                                 int b, int h, int j0, int lane, bool rope) {
   const int n = lane & 31, hh = lane >> 5;
+  const bool half = (a.flags & kRopeHalf) != 0;
+  float sc_nb[2];
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int nb = 0; nb < 2; ++nb) {
+    const int j = j0 + 32 * nb + n;
+    const int pos = a.pos0[b] + j;
+    const bool ok = j < a.T && (!rope || (pos >= 0 && pos < a.rope_positions));
+    const int64_t row = ((((int64_t)li * a.B + b) * a.T + j) * a.H + h) * kDim;
+    float xv[32];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int d = 32 * mb + 8 * (r >> 2) + (r & 3);
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[d]), __float_as_uint(x[d + 4]), false,
-                                                       false);
-      x[d] = __uint_as_float(sw[0]);       // token n, dimension d + 4h
-      x[d + 4] = __uint_as_float(sw[1]);   // token 32 + n, dimension d + 4h
+    for (int q = 0; q < 4; ++q) {
+      const int d0 = 16 * q + 8 * hh;
+      if (F16) {
+        uint4 w = make_uint4(0, 0, 0, 0);
+        if (ok) w = *reinterpret_cast<const uint4*>(reinterpret_cast<const __half*>(src) + row + d0);
+        const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          xv[8 * q + 2 * p] = half_bits_to_float(ww[p]);
+          xv[8 * q + 2 * p + 1] = half_bits_to_float(ww[p] >> 16);
+        }
+      } else {
+        float4 f0 = make_float4(0.0f, 0.0f, 0.0f, 0.0f), f1 = f0;
+        if (ok) {
+          f0 = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(src) + row + d0);
+          f1 = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(src) + row + d0 + 4);
+        }
+        xv[8 * q + 0] = f0.x; xv[8 * q + 1] = f0.y; xv[8 * q + 2] = f0.z; xv[8 * q + 3] = f0.w;
+        xv[8 * q + 4] = f1.x; xv[8 * q + 5] = f1.y; xv[8 * q + 6] = f1.z; xv[8 * q + 7] = f1.w;
+      }
     }
+    if (rope && ok) {
+      const float4* cs4 = reinterpret_cast<const float4*>(a.rope_cs + (int64_t)pos * 2 * kPairs);
+      if (!half) {
+        // pairs m = (16q + 8h)/2 + p, p = 0..3: (cos, sin) of two pairs per float4
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int pp = 0; pp < 2; ++pp) {
+            const float4 c = cs4[(16 * q + 8 * hh) / 4 + pp];
+            float* g = &xv[8 * q + 4 * pp];
+            const float x0 = g[0], x1 = g[1], x2 = g[2], x3 = g[3];
+            g[0] = x0 * c.x - x1 * c.y; g[1] = x0 * c.y + x1 * c.x;
+            g[2] = x2 * c.z - x3 * c.w; g[3] = x2 * c.w + x3 * c.z;
+          }
+      } else {
+        // pair (d, d + 32), d = 16q + 8h + j for q < 2, angle index d
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int j4 = 0; j4 < 4; ++j4) {
+            const float4 c = cs4[(16 * q + 8 * hh) / 2 + j4];   // (c, s) of d and d + 1
+#pragma unroll
+            for (int t2 = 0; t2 < 2; ++t2) {
+              const int jj = 2 * j4 + t2;
+              const float cc = t2 ? c.z : c.x, ss = t2 ? c.w : c.y;
+              const float xa = xv[8 * q + jj], xb = xv[8 * (q + 2) + jj];
+              xv[8 * q + jj] = xa * cc - xb * ss;
+              xv[8 * (q + 2) + jj] = xa * ss + xb * cc;
+            }
+          }
+      }
+    }
+    float m = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 32; ++k) m = fmaxf(m, fabsf(xv[k]));
+    m = fmaxf(m, __shfl_xor(m, 32, 64));   // the token's other 32 values sit in lane l ^ 32
+    sc_nb[nb] = unit_scale(m);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) split8(&xv[8 * q], sc_nb[nb], ops.hi[nb][q], ops.lo[nb][q]);
+  }
+  return hh ? sc_nb[1] : sc_nb[0];
+}
+
+// x^ of token j0 + lane in out[64] (Pi staged as fp16 parts).
+template <bool F16>
+__device__ __forceinline__ void rotate_tokens(float (&out)[kDim], const QuantArgs& a, const void* src,
+                                              const _Float16* pih, const _Float16* pil, int li, int b, int h,
+                                              int j0, int lane, bool rope) {
+  SplitOps ops;
+  const float sc = load_split_rows<F16>(ops, a, src, li, b, h, j0, lane, rope);
   f32x16 acc[2][2];
+  split_products(ops, pih, pil, lane, acc);
+  to_lane_per_token(acc, out);
+  const float inv = 1.0f / sc;   // a power of two: exact
 #pragma unroll
-  for (int r = 0; r < 16; ++r) { acc[0][0][r] = 0.0f; acc[1][0][r] = 0.0f; acc[0][1][r] = 0.0f; acc[1][1][r] = 0.0f; }
+  for (int d = 0; d < kDim; ++d) out[d] *= inv;
+}
+
+// Projected QJL sign bits of the wave's 64 residuals (lane l: r of token
+// j0 + l): bit i = !(p_i < 0) for p_i the binary32 fma chain over k
+// ascending of S[i][k] r_k (the exact quantizer step). p~ = (sigma_i S_i) .
+// (s r) comes from the matrix cores (sigma_i, s: the row's and the token's
+// power-of-two scales). Any evaluation of it there is within
+// 2^-17.3 ||sigma_i S_i|| ||s r|| of its exact value (2^-21 per split
+// product, the fp16 spacing below the unit-sized entries, and fp32 sums of
+// 64 terms) and the chain within 2^-18 of that, so where
+// |p~_i| > 2^-14 ||sigma_i S_i|| ||s r|| the signs agree; the coordinates
+// inside that band are recomputed with the chain from S in memory.
+// The residuals reach the B layout through v_permlane32_swap pairs
+// (16q + j, 16q + 8 + j) and go back the same way (a swap undoes itself).
+__device__ __forceinline__ uint64_t projected_signs(float (&x)[kDim], float g, const _Float16* sh,
+                                                    const _Float16* sl, const float* s_Sn, const float* S,
+                                                    int lane) {
+  const int hh = lane >> 5;
+  float m = 0.0f;
 #pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    int o = n * kPiPitch + 8 * q + 4 * hh;
-    asm volatile("" : "+v"(o));
-    const float4 p0 = *reinterpret_cast<const float4*>(s_S + o);
-    const float4 p1 = *reinterpret_cast<const float4*>(s_S + o + 32 * kPiPitch);
-    const float a0[4] = {p0.x, p0.y, p0.z, p0.w}, a1[4] = {p1.x, p1.y, p1.z, p1.w};
+  for (int k = 0; k < kDim; ++k) m = fmaxf(m, fabsf(x[k]));
+  const float sc = unit_scale(m);                    // token l's scale
+  const float sc_other = __shfl_xor(sc, 32, 64);     // token l ^ 32's
+  const float sc0 = hh ? sc_other : sc, sc1 = hh ? sc : sc_other;   // tokens n, 32 + n
+  SplitOps ops;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[j], x[8 * q + j], acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0[j], x[8 * q + 4 + j], acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[j], x[8 * q + j], acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1[j], x[8 * q + 4 + j], acc[1][1], 0, 0, 0);
+  for (int q = 0; q < 4; ++q) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[16 * q + j]),
+                                                       __float_as_uint(x[16 * q + 8 + j]), false, false);
+      x[16 * q + j] = __uint_as_float(sw[0]);       // token n, dimension 16q + 8h + j
+      x[16 * q + 8 + j] = __uint_as_float(sw[1]);   // token 32 + n, dimension 16q + 8h + j
+    }
+    split8(&x[16 * q], sc0, ops.hi[0][q], ops.lo[0][q]);
+    split8(&x[16 * q + 8], sc1, ops.hi[1][q], ops.lo[1][q]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[16 * q + j]),
+                                                       __float_as_uint(x[16 * q + 8 + j]), false, false);
+      x[16 * q + j] = __uint_as_float(sw[0]);
+      x[16 * q + 8 + j] = __uint_as_float(sw[1]);
     }
   }
-  // residuals back to one token per lane; p~ likewise
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int d = 32 * mb + 8 * (r >> 2) + (r & 3);
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[d]), __float_as_uint(x[d + 4]), false,
-                                                       false);
-      x[d] = __uint_as_float(sw[0]);
-      x[d + 4] = __uint_as_float(sw[1]);
-      const auto sp = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[mb][0][r]),
-                                                       __float_as_uint(acc[mb][1][r]), false, false);
-      acc[mb][0][r] = __uint_as_float(sp[0]);   // p~ of row d
-      acc[mb][1][r] = __uint_as_float(sp[1]);   // p~ of row d + 4
-    }
+  f32x16 acc[2][2];
+  split_products(ops, sh, sl, lane, acc);
+  float p[kDim];
+  to_lane_per_token(acc, p);
   uint64_t bits = 0, flagged = 0;
-  const float gb = g * 0x1p-14f;
+  const float gb = g * sc * 0x1p-14f;
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r)
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int i = 32 * mb + 8 * (r >> 2) + (r & 3) + 4 * half;
-        const float pv = acc[mb][half][r];
-        const bool sure = fabsf(pv) > s_Sn[i] * gb;
-        bits |= (uint64_t)((sure && !(pv < 0.0f)) ? 1u : 0u) << i;
-        flagged |= (uint64_t)(sure ? 0u : 1u) << i;
-      }
+  for (int i = 0; i < kDim; ++i) {
+    const bool sure = fabsf(p[i]) > s_Sn[i] * gb;
+    bits |= (uint64_t)((sure && !(p[i] < 0.0f)) ? 1u : 0u) << i;
+    flagged |= (uint64_t)(sure ? 0u : 1u) << i;
+  }
   // rows inside the band, any lane: the fixed-order chain (wave-uniform row)
   uint64_t any = flagged;
 #pragma unroll
@@ -252,7 +293,7 @@ __device__ __forceinline__ uint64_t projected_signs(float (&x)[kDim], float g, c
     const int i = __builtin_ctzll(any);
     any &= any - 1;
     if ((flagged >> i) & 1ull) {
-      const float4* row = reinterpret_cast<const float4*>(s_S + i * kPiPitch);
+      const float4* row = reinterpret_cast<const float4*>(S + i * kDim);
       float acc_i = 0.0f;
 #pragma unroll
       for (int k4 = 0; k4 < kDim / 4; ++k4) {
@@ -273,14 +314,16 @@ __device__ __forceinline__ uint64_t projected_signs(float (&x)[kDim], float g, c
 // x = ceil(T/256), y = B*H, z = nlayers. LDS: Pi (pitch 68) for the
 // rotations, S (row-major, read by the quantizer as broadcasts) and one
 // 64 x 8 word buffer per wave for the V transpose.
-// Three waves per SIMD (168 registers; a few values of the quantizer step
-// spill) run faster than two without spills: 312 against 343 us on the
-// 650M-shape prefill.
+// Three waves per SIMD (168 registers; a few values spill) run faster than
+// two without spills: 225 against 392 us on the 650M-shape prefill.
 template <bool F16, bool VQJL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void quantize_tiles_kernel(QuantArgs a) {
-  __shared__ __attribute__((aligned(16))) float s_pi[kDim * kPiPitch];
-  __shared__ __attribute__((aligned(16))) float s_S[kDim * kPiPitch];
-  __shared__ float s_Sn[kDim];                                       // ||S_i|| (fp32)
+  __shared__ __attribute__((aligned(16))) _Float16 s_pih[kDim * kHPitch];   // Pi, fp16 parts
+  __shared__ __attribute__((aligned(16))) _Float16 s_pil[kDim * kHPitch];
+  __shared__ __attribute__((aligned(16))) _Float16 s_sh[kDim * kHPitch];    // sigma_i S_i, fp16 parts
+  __shared__ __attribute__((aligned(16))) _Float16 s_sl[kDim * kHPitch];
+  __shared__ float s_Sn[kDim];                                               // ||sigma_i S_i||
+  __shared__ float s_sig[kDim];                                              // sigma_i
   __shared__ uint32_t s_vt[4][kDim * 8];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
@@ -291,17 +334,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   const bool paper = (a.flags & kQjlPaper) != 0;
   const int vsign = VQJL ? (paper ? 2 : 1) : 0;   // (a V sign pass is compiled only where asked for)
 
-  for (int e = threadIdx.x; e < kDim * kDim / 4; e += blockDim.x) {
-    const float4 pv = reinterpret_cast<const float4*>(a.pi + lh * kDim * kDim)[e];
-    *reinterpret_cast<float4*>(s_pi + (e >> 4) * kPiPitch + (e & 15) * 4) = pv;
-    *reinterpret_cast<float4*>(s_S + (e >> 4) * kPiPitch + (e & 15) * 4) =
-        reinterpret_cast<const float4*>(a.qjl_s)[e];
-  }
   if (threadIdx.x < kDim) {
+    // row i of S: its power-of-two scale and the norm of the scaled row
     const float* srow = a.qjl_s + threadIdx.x * kDim;
+    float mx = 0.0f;
+    for (int k = 0; k < kDim; ++k) mx = fmaxf(mx, fabsf(srow[k]));
+    const float sig = unit_scale(mx);
     float ss = 0.0f;
-    for (int k = 0; k < kDim; ++k) ss = fmaf(srow[k], srow[k], ss);
+    for (int k = 0; k < kDim; ++k) {
+      const float v = srow[k] * sig;
+      ss = fmaf(v, v, ss);
+    }
+    s_sig[threadIdx.x] = sig;
     s_Sn[threadIdx.x] = sqrtf(ss);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < kDim * kDim / 4; e += blockDim.x) {
+    const int r = e >> 4, c4 = (e & 15) * 4;
+    const float4 pv = reinterpret_cast<const float4*>(a.pi + lh * kDim * kDim)[e];
+    const float4 sv = reinterpret_cast<const float4*>(a.qjl_s)[e];
+    const float sig = s_sig[r];
+    const float pa[4] = {pv.x, pv.y, pv.z, pv.w};
+    const float sa[4] = {sv.x * sig, sv.y * sig, sv.z * sig, sv.w * sig};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const _Float16 ph = (_Float16)pa[u], sh = (_Float16)sa[u];
+      s_pih[r * kHPitch + c4 + u] = ph;
+      s_pil[r * kHPitch + c4 + u] = (_Float16)(pa[u] - (float)ph);
+      s_sh[r * kHPitch + c4 + u] = sh;
+      s_sl[r * kHPitch + c4 + u] = (_Float16)(sa[u] - (float)sh);
+    }
   }
   const Levels Lk = load_levels(a.lut_k + lh * 8);
   const Levels Lv = load_levels(a.lut_v + lh * 8);
@@ -327,12 +389,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
 #pragma unroll
     for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.k, row + i, false) : 0.0f;
   } else {
-    rotate_tokens<F16>(x, a, a.k, s_pi, li, b, h, j0, lane, true);
+    rotate_tokens<F16>(x, a, a.k, s_pih, s_pil, li, b, h, j0, lane, true);
   }
   uint32_t kw[8];
-  const QuantOut qk = quantize_lane<true>(x, Lk, s_S, paper ? 2 : 3, kw);
+  const QuantOut qk = quantize_lane<true>(x, Lk, nullptr, paper ? 2 : 3, kw);
   if (!paper) {
-    const uint64_t sb = projected_signs(x, qk.g, s_S, s_Sn, lane);
+    const uint64_t sb = projected_signs(x, qk.g, s_sh, s_sl, s_Sn, a.qjl_s, lane);
 #pragma unroll
     for (int w = 0; w < 8; ++w) kw[w] |= (uint32_t)((sb >> (8 * w)) & 0xFFu) << 24;
   }
@@ -347,15 +409,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   // are not hoisted above the key's stores (registers, occupancy).
   asm volatile("" ::: "memory");
   if (!rotated && (a.flags & kVRotate)) {
-    rotate_tokens<F16>(x, a, a.v, s_pi, li, b, h, j0, lane, false);
+    rotate_tokens<F16>(x, a, a.v, s_pih, s_pil, li, b, h, j0, lane, false);
   } else {
 #pragma unroll
     for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.v, row + i, F16) : 0.0f;
   }
   uint32_t vw[8];
-  const QuantOut qv = quantize_lane<false>(x, Lv, s_S, (VQJL && !paper) ? 3 : vsign, vw);
+  const QuantOut qv = quantize_lane<false>(x, Lv, nullptr, (VQJL && !paper) ? 3 : vsign, vw);
   if (VQJL && !paper) {
-    const uint64_t sb = projected_signs(x, qv.g, s_S, s_Sn, lane);
+    const uint64_t sb = projected_signs(x, qv.g, s_sh, s_sl, s_Sn, a.qjl_s, lane);
 #pragma unroll
     for (int i = 0; i < kDim; ++i) vw[i >> 3] |= (uint32_t)((sb >> i) & 1ull) << (4 * (i & 7) + 3);
   }
