@@ -12,6 +12,10 @@
  *   decode   (Sec. 3.1 decode steps 1-4, Algorithm 1 of Sec. 4.3):
  *       one pass over the packed cache: dequantize through the tables in
  *       registers, add the QJL score correction, online softmax, accumulate V.
+ * Entry points: tq_quantize_pack (prefill and appends), tq_decode_attend,
+ * tq_decode_step (append + attend in one launch), tq_dequantize (fp16 rows
+ * for a dequantize-then-attend path), tq_calibrate_rotation and
+ * tq_calibrate_lut (Sec. 3.2-3.3), tq_rope_table and sizing helpers.
  *
  * Every entry point is asynchronous on the HIP stream it is given and never
  * synchronizes. Device pointers are plain device addresses (hipMalloc or
