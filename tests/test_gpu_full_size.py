@@ -172,6 +172,23 @@ def test_full_650m_33layer_step():
     samples = [(l, h, j, j, k[l, 0, j, h], v[l, 0, j, h])
                for (l, _, h) in units[:8] for j in (0, 63, 64, 777, T - 1, T)]
     _check_codes(cache, samples, cs_host, pi, lut_k, lut_v, S, tq.V_ROTATE)
+    # the two-step baseline at this size: fp32 softmax attention over the
+    # dequantized fp16 rows reproduces the fused step's output to within the
+    # bound the rows' fp16 rounding implies (see tests/test_gpu_dequant.py)
+    ko, vo = tq.dequantize(params, cache, _i64([0]), _i32([T + 1]), T + 1, lk_d, lv_d, S_d)
+    torch.cuda.synchronize()
+    for (l, b, h) in units[:12]:
+        kk = ko[l, b, h].float().cpu().numpy().astype(np.float64)
+        vv = vo[l, b, h].float().cpu().numpy().astype(np.float64)
+        qr = oracle.rope_apply(q[l, b, h].astype(np.float32), T, cs_host)
+        P = pi[l, h].astype(np.float64)
+        qh = P @ qr
+        logits = 0.125 * (kk @ qh)
+        w = np.exp(logits - logits.max())
+        o = P.T @ ((w[:, None] * vv).sum(0) / w.sum())
+        d = 0.125 * np.abs(qh) @ (fp16_ulp(kk).T / 2)
+        bound = (np.exp(2 * d.max()) - 1) * np.abs(vv).max() + fp16_ulp(np.abs(vv).max()) + TOL
+        assert np.max(np.abs(o - out32[l, b, h])) <= bound, ((l, b, h), np.max(np.abs(o - out32[l, b, h])))
 
 
 def test_full_ragged_b64_step():
