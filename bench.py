@@ -58,7 +58,7 @@ def parse():
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
               "(every (sequence, layer, head) unit is independent, so heads or sequences would shard across GPUs with no communication).",
               file=sys.stderr)
         sys.exit(2)
