@@ -15,8 +15,10 @@
 // computes one 32-token x 32-dimension block, holding its column block of
 // S_hi and S_lo in registers for all the tiles the block covers. Everything
 // else is a table look-up and a scale. The tile's codes and scalars are staged
-// in LDS (the next tile's are loaded while the current one is computed), the
-// fp16 rows are assembled in LDS and written with 16-byte stores.
+// in LDS (the next tile's are loaded while the current one is computed), and
+// so are the estimates; a thread then writes 16 dimensions of a key row with
+// two 16-byte stores, and the value rows (dimension-major codes) are
+// transposed through LDS before their 16-byte stores.
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
 
@@ -27,14 +29,6 @@ namespace {
 constexpr int kTilesPerBlock = 4;
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-// c[i & 7] by three levels of selects (a register table, never memory).
-__device__ __forceinline__ float pick8(const float (&c)[8], uint32_t i) {
-  const bool b0 = (i & 1u) != 0, b1 = (i & 2u) != 0, b2 = (i & 4u) != 0;
-  const float p01 = b0 ? c[1] : c[0], p23 = b0 ? c[3] : c[2];
-  const float p45 = b0 ? c[5] : c[4], p67 = b0 ? c[7] : c[6];
-  const float p03 = b1 ? p23 : p01, p47 = b1 ? p67 : p45;
-  return b2 ? p47 : p03;
-}
 
 }  // namespace
 
@@ -70,8 +64,10 @@ __global__ __launch_bounds__(256) void dequant_kernel(DequantArgs a) {
   __shared__ __attribute__((aligned(16))) uint4 s_k[128];      // K tile: chunk (c, r) at c*64 + r
   __shared__ __attribute__((aligned(16))) uint4 s_v[128];      // V tile: chunk (c, i) at c*64 + i
   __shared__ __attribute__((aligned(16))) uint2 s_sc[64];      // [n_k | g_k, n_v | g_v] per slot
-  __shared__ __attribute__((aligned(16))) __half s_ok[64 * 64];  // k~ rows of the tile
+  __shared__ __attribute__((aligned(16))) float s_ek[64 * 64];                 // key estimates e[t][c]
+  __shared__ __attribute__((aligned(16))) float s_ev[VQJL ? 64 * 64 : 1];   // value estimates
   __shared__ __attribute__((aligned(16))) __half s_ov[64 * 64];  // v~ rows of the tile
+  __shared__ float s_lk[8], s_lv[8];                             // the tables
 
   const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
   const int n = lane & 31, hh = lane >> 5;
@@ -95,15 +91,10 @@ __global__ __launch_bounds__(256) void dequant_kernel(DequantArgs a) {
 
   const bool paper = (a.flags & kQjlPaper) != 0;
   constexpr bool vqjl = VQJL;   // (the V sign pass is compiled only where asked for)
-  float ck[8], cv[8];
-#pragma unroll
-  for (int m = 0; m < 8; ++m) { ck[m] = a.lut_k[lh * 8 + m]; cv[m] = a.lut_v[lh * 8 + m]; }
-  // pinned in registers: a select between elements of a table in an array
-  // would otherwise be folded into an indexed load from private memory
-  asm volatile("" : "+v"(ck[0]), "+v"(ck[1]), "+v"(ck[2]), "+v"(ck[3]), "+v"(ck[4]), "+v"(ck[5]),
-               "+v"(ck[6]), "+v"(ck[7]));
-  asm volatile("" : "+v"(cv[0]), "+v"(cv[1]), "+v"(cv[2]), "+v"(cv[3]), "+v"(cv[4]), "+v"(cv[5]),
-               "+v"(cv[6]), "+v"(cv[7]));
+  if (t < 8) {
+    s_lk[t] = a.lut_k[lh * 8 + t];
+    s_lv[t] = a.lut_v[lh * 8 + t];
+  }
   const float ebar_k = paper ? a.ebar[lh * 2] : 0.0f;
   const float ebar_v = paper ? a.ebar[lh * 2 + 1] : 0.0f;
   // this lane's B operands: S[16q + 8h + j][32 nb + n] as S_hi + S_lo
@@ -167,48 +158,87 @@ __global__ __launch_bounds__(256) void dequant_kernel(DequantArgs a) {
       }
     }
 
-    // ---- rows: register r holds token 32 mb + 8 (r/4) + 4h + r%4, dimension c
-    // (the row base is re-derived per tile: the empty asm keeps the compiler
-    // from holding every row's addresses across the tile loop)
-    const uint32_t* kw = reinterpret_cast<const uint32_t*>(s_k);
-    const uint32_t* vw = reinterpret_cast<const uint32_t*>(s_v);
-    int trb = 32 * mb + 4 * hh;
-    asm volatile("" : "+v"(trb));
+    // ---- the estimates to LDS: register r holds token 32 mb + 8 (r/4) + 4h + r%4,
+    // dimension c (consecutive dimensions across a half wave: no conflicts)
+    if (!paper) {
+      int trb = 32 * mb + 4 * hh;
+      asm volatile("" : "+v"(trb));
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int tr = trb + 8 * (r >> 2) + (r & 3);
-      const uint2 sc = s_sc[tr];
-      const float nk = half_bits_to_float(sc.x), gk = half_bits_to_float(sc.x >> 16);
-      const float nv = half_bits_to_float(sc.y), gv = half_bits_to_float(sc.y >> 16);
-      // key word c/8 of token tr: chunk c/32 = nb, word (c/8) % 4
-      const uint32_t kword = kw[(nb * 64 + tr) * 4 + ((c >> 3) & 3)];
-      const uint32_t kidx = (kword >> (3 * (c & 7))) & 7u;
-      const float ksg = ((kword >> (24 + (c & 7))) & 1u) ? 1.0f : -1.0f;
-      float kv = pick8(ck, kidx);
-      kv += paper ? ebar_k * ksg : (kQjlAlpha * gk) * ek[r];
-      // value nibble of token tr, dimension c
-      const uint32_t vword = vw[((tr >> 5) * 64 + c) * 4 + ((tr >> 3) & 3)];
-      const uint32_t vnib = (vword >> (4 * (tr & 7))) & 15u;
-      float vv = pick8(cv, vnib);
-      if (vqjl) {
-        const float vsg = (vnib >> 3) ? 1.0f : -1.0f;
-        vv += paper ? ebar_v * vsg : (kQjlAlpha * gv) * ev[r];
+      for (int r = 0; r < 16; ++r) {
+        const int tr = trb + 8 * (r >> 2) + (r & 3);
+        s_ek[tr * kDim + c] = ek[r];
+        if constexpr (VQJL) s_ev[tr * kDim + c] = ev[r];
       }
-      s_ok[tr * kDim + c] = __float2half_rn(kv * (nk * 0.125f));
-      s_ov[tr * kDim + c] = __float2half_rn(vv * (nv * 0.125f));
-      if ((r & 3) == 3) asm volatile("" ::: "memory");   // four rows' reads at a time (registers)
     }
     __syncthreads();
 
-    // ---- 16-byte stores of the tile's valid rows (the staging is rewritten
-    // only after the next iteration's first barrier)
     const int rows = min(64, len - 64 * tt);
+    // ---- key rows: thread t writes dimensions 16g .. 16g + 15 (g = t % 4) of
+    // token t / 4 straight to memory (two 16-byte stores)
+    {
+      const int tk = t >> 2, g = t & 3;
+      const uint2 sc = s_sc[tk];
+      const float nk8 = half_bits_to_float(sc.x) * 0.125f, gk = half_bits_to_float(sc.x >> 16);
+      const float coef = paper ? ebar_k : kQjlAlpha * gk;
+      const uint32_t* kw = reinterpret_cast<const uint32_t*>(s_k);
+      uint32_t packed[8];
+#pragma unroll
+      for (int half16 = 0; half16 < 2; ++half16) {
+        const int w = 2 * g + half16;                                  // key word: dims 8w .. 8w + 7
+        const uint32_t word = kw[((w >> 2) * 64 + tk) * 4 + (w & 3)];
+        const float4 e0 = paper ? make_float4(0.f, 0.f, 0.f, 0.f)
+                                : *reinterpret_cast<const float4*>(s_ek + tk * kDim + 8 * w);
+        const float4 e1 = paper ? make_float4(0.f, 0.f, 0.f, 0.f)
+                                : *reinterpret_cast<const float4*>(s_ek + tk * kDim + 8 * w + 4);
+        const float ee[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+#pragma unroll
+        for (int j = 0; j < 8; j += 2) {
+          float kv[2];
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const uint32_t idx = (word >> (3 * (j + u))) & 7u;
+            const float e = paper ? (((word >> (24 + j + u)) & 1u) ? 1.0f : -1.0f) : ee[j + u];
+            kv[u] = (s_lk[idx] + coef * e) * nk8;
+          }
+          packed[4 * half16 + j / 2] = (uint32_t)__half_as_ushort(__float2half_rn(kv[0])) |
+                                       ((uint32_t)__half_as_ushort(__float2half_rn(kv[1])) << 16);
+        }
+      }
+      if (tk < rows) {
+        __half* dst = ko + ((int64_t)64 * tt + tk) * kDim + 16 * g;
+        reinterpret_cast<uint4*>(dst)[0] = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+        reinterpret_cast<uint4*>(dst)[1] = make_uint4(packed[4], packed[5], packed[6], packed[7]);
+      }
+    }
+    // ---- value rows: thread t reads dimension i = t % 64's words of tokens
+    // 16 (t / 64) .. + 15 and stages the 16 values in LDS
+    {
+      const int i = t & 63, tg = t >> 6;
+      const uint32_t* vw = reinterpret_cast<const uint32_t*>(s_v);
+#pragma unroll
+      for (int w2 = 0; w2 < 2; ++w2) {
+        const int t0 = 16 * tg + 8 * w2;                               // tokens t0 .. t0 + 7
+        const uint32_t word = vw[((t0 >> 5) * 64 + i) * 4 + ((t0 >> 3) & 3)];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int tv = t0 + j;
+          const uint32_t nib = (word >> (4 * j)) & 15u;
+          const uint2 sc = s_sc[tv];
+          float vv = s_lv[nib & 7u];
+          if constexpr (VQJL) {
+            const float sg = (nib >> 3) ? 1.0f : -1.0f;
+            vv += paper ? ebar_v * sg : (kQjlAlpha * half_bits_to_float(sc.y >> 16)) * s_ev[tv * kDim + i];
+          }
+          s_ov[tv * kDim + i] = __float2half_rn(vv * (half_bits_to_float(sc.y) * 0.125f));
+        }
+      }
+    }
+    __syncthreads();
 #pragma unroll
     for (int e0 = 0; e0 < 512; e0 += 256) {
       const int e = e0 + t, row = e >> 3, col = (e & 7) * 8;
       if (row < rows) {
         const int64_t j = (int64_t)64 * tt + row;
-        *reinterpret_cast<uint4*>(ko + j * kDim + col) = *reinterpret_cast<const uint4*>(s_ok + row * kDim + col);
         *reinterpret_cast<uint4*>(vo + j * kDim + col) = *reinterpret_cast<const uint4*>(s_ov + row * kDim + col);
       }
     }
