@@ -15,7 +15,8 @@
  * Entry points: tq_quantize_pack (prefill and appends), tq_decode_attend,
  * tq_decode_step (append + attend in one launch), tq_dequantize (fp16 rows
  * for a dequantize-then-attend path), tq_calibrate_rotation and
- * tq_calibrate_lut (Sec. 3.2-3.3), tq_rope_table and sizing helpers.
+ * tq_calibrate_lut (Sec. 3.2-3.3), tq_calibrate_ebar (Sec. 3.4), tq_rope_table
+ * and sizing helpers.
  *
  * Every entry point is asynchronous on the HIP stream it is given and never
  * synchronizes. Device pointers are plain device addresses (hipMalloc or
@@ -25,7 +26,13 @@
  * the call returns a negative tq_status and tq_last_error() returns a
  * thread-local message. Device code never traps; per-sequence metadata held
  * in device memory is checked by the kernels, which skip what is out of range
- * as documented per entry point.
+ * as documented per entry point. Tables of levels held in device memory
+ * (lut_k, lut_v) must be strictly ascending, since the midpoint rule of the
+ * quantizer assumes it; the kernels check each (layer, head)'s pair of tables
+ * when they load them: a quantize call does not write a (layer, head) whose
+ * K or V table is not strictly ascending (or holds a NaN), tq_dequantize skips
+ * it, and decode writes NaN to its output (the host-side equivalent of
+ * TQ_ERR_LUT_ORDER, which host tables such as tq_calibrate_lut's init get).
  *
  * Fixed layout facts (head_dim must be 64):
  *   - code words: a token-head vector of 64 codes is 32 bytes, eight 32-bit
@@ -160,7 +167,8 @@ TQ_API tq_status tq_rope_table(float* cs, int32_t positions, double base, void* 
  *          Tokens whose slot falls outside [0, slots) or whose position
  *          falls outside [0, rope_positions) are not written.
  *   pi     device [L][H][64][64] fp32, row-major, x^ = pi . x (absolute layer).
- *   lut_k, lut_v  device [L][H][8] fp32, strictly ascending.
+ *   lut_k, lut_v  device [L][H][8] fp32, strictly ascending (a (layer, head)
+ *          whose pair of tables is not is not written).
  *   qjl_s  device [64][64] fp32 Gaussian projection S (ignored with TQ_QJL_PAPER).
  *   ebar   unused by the quantizer (may be NULL).
  */
@@ -187,14 +195,18 @@ TQ_API tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache
  *   q_pos   device int32 [B]: RoPE position of the query.
  *   seq_slot0 device int64 [B]: first slot of each sequence, multiple of 64.
  *   seq_len device int32 [B]: cached tokens, 0 <= seq_len <= max_len.
- *           A sequence whose range or query position is invalid gets NaN output.
+ *           A sequence whose range or query position is invalid gets NaN
+ *           output, and so does a (layer, head) whose lut_k or lut_v is not
+ *           strictly ascending.
  *   max_len host bound on every seq_len (sizes the split-K grid), >= 0.
  *   out     device [nlayers][B][H][64]: io_dtype, or fp32 with TQ_OUT_FP32.
  *   workspace device, >= tq_decode_workspace_bytes(...) bytes, 16-byte aligned
  *           (NULL when that is 0). When long sequences are split across
  *           blocks it holds the split partials and one counter per unit; it
- *           must be zero-filled before its first use, and every call leaves
- *           the counters at zero again.
+ *           must be zero-filled before its first use, and every call that
+ *           completes leaves all of it zero again (the split that merges
+ *           clears the partials it read and the counter), so one zero-filled
+ *           workspace serves later calls of any shape.
  *           Calls that share a workspace must be ordered on one stream.
  */
 TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache,
@@ -223,7 +235,13 @@ TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache
  *           goes to slot seq_slot0[b] + seq_len[b] and the step attends over
  *           seq_len[b] + 1 tokens. The caller advances its own lengths.
  *           A sequence that would exceed max_len, its slot range or the RoPE
- *           table is not appended and gets NaN output.
+ *           table is not appended and gets NaN output (as does a (layer,
+ *           head) whose lut_k or lut_v is not strictly ascending).
+ *           The block's waves that score the new token's tile wait, bounded,
+ *           for the block's own waves that append it (they wait on nothing,
+ *           so the bound is never reached in practice); if the wait gives
+ *           up, that unit's output is NaN (the appended codes are in the
+ *           cache). tq_set_step_wait_limit sets the bound.
  *   max_len host bound on every seq_len[b] + 1, >= 1.
  *   pi, lut_k, lut_v, qjl_s, ebar, out: as tq_decode_attend.
  *   workspace as tq_decode_attend, >= tq_decode_workspace_bytes(params, B,
@@ -241,7 +259,7 @@ TQ_API tq_status tq_decode_step(const tq_params* params, const tq_cache* cache,
 
 /* Dequantize the cache into plain fp16 key and value rows: the first step of
  * a "dequantize first, then attend" path, the comparison the paper makes for
- * its fused kernel (Sec. 5.4, Table 6: unpack to full precision, then
+ * its fused kernel (Sec. 5.3, Table 6: unpack to full precision, then
  * attention). For every layer, sequence b and head, token j < seq_len[b]:
  *   k~_j = (n_k,j/8) ( c_K[idx_j] + alpha g_k,j S^T (2 s_j - 1) )
  *          (TQ_QJL_PAPER: ebar_K (2 s_j - 1) in place of alpha g_k,j S^T (2 s_j - 1))
@@ -252,7 +270,8 @@ TQ_API tq_status tq_decode_step(const tq_params* params, const tq_cache* cache,
  * o^ is the softmax-weighted mean of the v~_j (before Pi^T).
  *
  *   seq_slot0, seq_len  device [B], as tq_decode_attend; a sequence whose
- *           range is invalid (or seq_len > max_len) is skipped.
+ *           range is invalid (or seq_len > max_len) is skipped, and so is a
+ *           (layer, head) whose lut_k or lut_v is not strictly ascending.
  *   max_len host: the token stride of the outputs, >= every seq_len.
  *   lut_k, lut_v, qjl_s, ebar  as tq_decode_attend (qjl_s may be NULL with
  *           TQ_QJL_PAPER; ebar is needed only then).
@@ -303,6 +322,34 @@ TQ_API tq_status tq_calibrate_rotation(const float* x, int32_t nheads, int32_t n
 TQ_API tq_status tq_calibrate_lut(const float* x, int32_t nheads, int32_t ncal, const float* pi,
                            const float* init, int32_t max_iter, double tol, float* lut_out,
                            void* stream);
+
+/* Per-head mean absolute residual ebar of the per-element residual form
+ * (TQ_QJL_PAPER; Sec. 3.4, Eq. 7: the correction adds sign(r_i) ebar): over
+ * every normalized coordinate u = 8 x^ / ||x^|| of the head's calibration
+ * vectors (x^ = Pi x in fp64, x^ = x when pi is NULL; a zero vector gives
+ * zeros, as in the quantizer),
+ *   ebar = mean over vectors and coordinates of |u - c[idx(u)]|,
+ *   idx(u) = #{m : u > (c_m + c_{m+1})/2}   (fp64 midpoints),
+ * with the head's table c, summed in fp64. Call it once with post-RoPE keys
+ * and lut_k for ebar_K and once with values and lut_v for ebar_V.
+ *   x        device [nheads][ncal][64] fp32.
+ *   pi       device [nheads][64][64] fp32 rotations, or NULL.
+ *   lut      device [nheads][8] fp32, strictly ascending (a head whose table
+ *            is not gets NaN).
+ *   ebar_out device fp32: head h's value goes to element h * stride (stride 2
+ *            with ebar_out = ebar or ebar + 1 fills the K or V column of the
+ *            [L][H][2] array the decode entry points take).
+ *   stride   >= 1. */
+TQ_API tq_status tq_calibrate_ebar(const float* x, int32_t nheads, int32_t ncal, const float* pi,
+                                   const float* lut, float* ebar_out, int32_t stride, void* stream);
+
+/* Bound, in polls of about 64 clock cycles each, of the wait inside a
+ * tq_decode_step block for the two waves that append the new token (default
+ * 4194304, restored by a negative limit). For tests of the failure path: a
+ * limit of 0 makes every wait give up at once, so every unit of a step whose
+ * new token is scored gets NaN output. Process-wide; it applies to launches
+ * made after the call. Returns the previous limit. */
+TQ_API int32_t tq_set_step_wait_limit(int32_t limit);
 
 /* Message of the last failing call on this thread ("" if none). */
 TQ_API const char* tq_last_error(void);

@@ -13,6 +13,7 @@ Contents
     lloyd_max_gaussian  3-bit Lloyd-Max levels for N(0, 1)     (Sec. 3.3, Eq. 5)
     kmeans_1d           1-D Lloyd iteration on samples          (Sec. 4.1, LUT calibration)
     calibrate_rotation  Pi = V^T of the SVD of post-RoPE keys   (Sec. 3.2)
+    calibrate_ebar      per-head mean |u - c(u)| of a table      (Sec. 3.4, Eq. 7)
     qjl_estimate        sqrt(pi/2)/m ||r|| <S y, sign(S r)>     (Sec. 3.4, projected form)
     paper_memory_table  the accounting of Table 4               (Sec. 5.2)
 Parity status: all functions are pinned by ``tests/test_oracle_*.py``.
@@ -317,6 +318,17 @@ def calibrate_lut(x, pi, init, max_iter: int = 100, tol: float = 1e-7) -> np.nda
     1-D Lloyd iteration of kmeans_1d on every normalized coordinate of the
     calibration vectors x [n][64] (rotated by pi unless None)."""
     return kmeans_1d(normalized_coordinates(x, pi).reshape(-1), init, max_iter, tol)
+
+
+def calibrate_ebar(x, pi, lut) -> float:
+    """Per-head mean absolute residual ebar of the per-element residual
+    correction (Sec. 3.4, Eq. 7; the correction adds sign(r_i) ebar): the mean
+    of |u - c[idx(u)]| over every normalized coordinate u of the calibration
+    vectors x [n][64] (rotated by pi unless None), idx by the midpoint rule of
+    assign_levels, fp64 throughout."""
+    u = normalized_coordinates(x, pi).reshape(-1)
+    c = np.asarray(lut, dtype=np.float64)
+    return float(np.mean(np.abs(u - c[assign_levels(u, c)])))
 
 
 # --------------------------------------------------------------------------

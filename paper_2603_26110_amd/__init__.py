@@ -7,7 +7,8 @@ raise ``RuntimeError`` (there is no fallback path).
 
 Entry points (same names as the C ABI without the ``tq_`` prefix):
     rope_table, quantize_pack, decode_attend, decode_step, dequantize,
-    decode_workspace_bytes, calibrate_rotation, calibrate_lut, cache_bytes, last_error, version
+    decode_workspace_bytes, calibrate_rotation, calibrate_lut, calibrate_ebar, set_step_wait_limit,
+    cache_bytes, last_error, version
 """
 from __future__ import annotations
 
@@ -19,7 +20,8 @@ import torch
 
 __all__ = [
     "Params", "Cache", "TQError", "rope_table", "quantize_pack", "decode_attend", "decode_step", "dequantize",
-    "decode_workspace_bytes", "calibrate_rotation", "calibrate_lut", "cache_bytes", "last_error", "version",
+    "decode_workspace_bytes", "calibrate_rotation", "calibrate_lut", "calibrate_ebar", "set_step_wait_limit",
+    "cache_bytes", "last_error", "version",
     "V_ROTATE", "V_QJL", "QJL_PAPER", "ROPE_HALF", "INPUT_ROTATED", "OUT_FP32", "lib_path",
 ]
 
@@ -78,6 +80,10 @@ def _load():
     L.tq_calibrate_lut.argtypes = [P, i32, i32, P, P, i32, ctypes.c_double, P, P]
     L.tq_calibrate_lut.restype = i32
     L.tq_calibrate_rotation.restype = i32
+    L.tq_calibrate_ebar.argtypes = [P, i32, i32, P, P, P, i32, P]
+    L.tq_calibrate_ebar.restype = i32
+    L.tq_set_step_wait_limit.argtypes = [i32]
+    L.tq_set_step_wait_limit.restype = i32
     _lib = L
     return L
 
@@ -315,6 +321,43 @@ def calibrate_lut(x: torch.Tensor, pi=None, init=None, max_iter: int = 100,
     _check(L.tq_calibrate_lut(_ptr(x), nh, ncal, _ptr(pi), ctypes.cast(init_arr, ctypes.c_void_p),
                               int(max_iter), float(tol), _ptr(out), _stream(x.device)))
     return out
+
+
+def calibrate_ebar(x: torch.Tensor, lut: torch.Tensor, pi=None, out=None, stride: int = 1) -> torch.Tensor:
+    """x: [nheads][ncal][64] fp32 calibration vectors (post-RoPE keys with
+    lut_k, or values with lut_v), lut: [nheads][8] tables, pi: [nheads][64][64]
+    rotations or None. Returns the per-head mean absolute residual; with a
+    contiguous fp32 ``out`` and ``stride`` the value of head h is written to
+    out.view(-1)[h * stride] (e.g. out = ebar.view(-1)[1:] and stride 2 fill
+    the V column of an [L][H][2] array), else a new [nheads] tensor."""
+    L = _load()
+    _dev(x, "x", torch.float32)
+    if x.dim() != 3 or x.shape[-1] != 64:
+        raise ValueError("x must be [nheads][ncal][64]")
+    nh, ncal = x.shape[:2]
+    _dev(lut, "lut", torch.float32)
+    if tuple(lut.shape) != (nh, 8):
+        raise ValueError("lut must be [nheads][8]")
+    if pi is not None:
+        _dev(pi, "pi", torch.float32)
+        if tuple(pi.shape) != (nh, 64, 64):
+            raise ValueError("pi must be [nheads][64][64]")
+    if out is None:
+        out = torch.empty(nh, dtype=torch.float32, device=x.device)
+        stride = 1
+    else:
+        _dev(out, "out", torch.float32)
+    if stride < 1 or out.numel() < (nh - 1) * stride + 1:
+        raise ValueError("out is too small for nheads at this stride")
+    _check(L.tq_calibrate_ebar(_ptr(x), nh, ncal, _ptr(pi), _ptr(lut), _ptr(out), int(stride),
+                               _stream(x.device)))
+    return out
+
+
+def set_step_wait_limit(limit: int) -> int:
+    """Bound of a decode step's wait for its appends (tests of the failure
+    path; a negative limit restores the default). Returns the previous one."""
+    return int(_load().tq_set_step_wait_limit(int(limit)))
 
 
 def calibrate_rotation(x: torch.Tensor):

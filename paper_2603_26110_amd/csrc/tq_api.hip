@@ -2,6 +2,7 @@
 // entry point validates its arguments before launching anything, returns a
 // negative tq_status on failure and records a thread-local message.
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -13,6 +14,7 @@
 namespace {
 
 thread_local char g_err[512] = "";
+std::atomic<int> g_wait_limit{tq::kDefaultWaitLimit};
 
 tq_status fail(tq_status code, const char* fmt, ...) {
   va_list ap;
@@ -68,6 +70,11 @@ tq_status check_cache(const tq_cache* c) {
 extern "C" {
 
 const char* tq_last_error(void) { return g_err; }
+
+int32_t tq_set_step_wait_limit(int32_t limit) {
+  if (limit < 0) limit = tq::kDefaultWaitLimit;
+  return g_wait_limit.exchange(limit, std::memory_order_relaxed);
+}
 
 const char* tq_version(void) { return "turboesm-gfx950 0.1.0"; }
 
@@ -188,6 +195,7 @@ tq_status decode_common(const tq_params* params, const tq_cache* cache, const vo
   a.out = out;
   a.nsplit = nsplit; a.split_tiles = split_tiles;
   a.k_new = k; a.v_new = v; a.append = step ? 1 : 0; a.len_add = step ? 1 : 0;
+  a.wait_limit = g_wait_limit.load(std::memory_order_relaxed);
   char* ws = (char*)workspace;
   if (nsplit > 1) {
     a.partials = (float*)ws;
@@ -282,6 +290,18 @@ tq_status tq_calibrate_lut(const float* x, int32_t nheads, int32_t ncal, const f
   return hip_status(tq::launch_calibrate_lut(x, nheads, ncal, pi, init, max_iter, tol, lut_out,
                                              (hipStream_t)stream),
                     "tq_calibrate_lut launch");
+}
+
+tq_status tq_calibrate_ebar(const float* x, int32_t nheads, int32_t ncal, const float* pi, const float* lut,
+                            float* ebar_out, int32_t stride, void* stream) {
+  if (nheads < 0 || ncal < 0) return fail(TQ_ERR_ARG, "nheads and ncal must be >= 0");
+  if (stride < 1) return fail(TQ_ERR_ARG, "stride must be >= 1");
+  if (nheads == 0) return ok();
+  if (!x || !lut || !ebar_out) return fail(TQ_ERR_ARG, "x, lut and ebar_out must not be NULL");
+  if (ncal == 0) return fail(TQ_ERR_ARG, "ncal must be positive");
+  if (nheads > 65535 * 1024) return fail(TQ_ERR_ARG, "too many heads");
+  return hip_status(tq::launch_calibrate_ebar(x, nheads, ncal, pi, lut, ebar_out, stride, (hipStream_t)stream),
+                    "tq_calibrate_ebar launch");
 }
 
 }  // extern "C"

@@ -297,4 +297,82 @@ hipError_t launch_calibrate_lut(const float* x, int nheads, int ncal, const floa
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- ebar
+// Per-head mean absolute residual of the per-element correction (Sec. 3.4,
+// Eq. 7): over every normalized coordinate u = 8 x^ / ||x^|| of the head's
+// calibration vectors (computed as in calibrate_lut_kernel), the mean of
+// |u - c[idx]| with idx = #{m : u > (c_m + c_{m+1})/2} (fp64 midpoints of the
+// fp32 levels). Each lane sums its coordinates in fp64 in vector order; the
+// 256 lane sums are added in a fixed order. A head whose table is not
+// strictly ascending gets NaN.
+struct EbarSmem {
+  double pi[kDim * kPiPitch];
+  double xv[kLutWaves][kDim];
+  double red[256];
+};
+
+__global__ __launch_bounds__(256) void calibrate_ebar_kernel(const float* x, int ncal, const float* pi,
+                                                             const float* lut, float* ebar_out, int stride) {
+  __shared__ EbarSmem sm;
+  const int head = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float* X = x + (int64_t)head * ncal * kDim;
+  const bool rot = pi != nullptr;
+  if (rot) {
+    const float* P = pi + (int64_t)head * kDim * kDim;
+    for (int e = t; e < kDim * kDim; e += 256) sm.pi[(e >> 6) * kPiPitch + (e & 63)] = (double)P[e];
+  }
+  double c[8];
+#pragma unroll
+  for (int m = 0; m < 8; ++m) c[m] = (double)lut[(int64_t)head * 8 + m];
+  bool asc = true;
+#pragma unroll
+  for (int m = 0; m < 7; ++m) asc = asc && (c[m] < c[m + 1]);
+  double th[7];
+#pragma unroll
+  for (int m = 0; m < 7; ++m) th[m] = 0.5 * (c[m] + c[m + 1]);
+  __syncthreads();
+  double acc = 0.0;
+  for (int v = wave; v < ncal; v += kLutWaves) {
+    const double xi = (double)X[(int64_t)v * kDim + lane];
+    double xh = xi;
+    if (rot) {
+      sm.xv[wave][lane] = xi;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      const double* row = sm.pi + lane * kPiPitch;
+      xh = 0.0;
+#pragma unroll 8
+      for (int k = 0; k < kDim; ++k) xh = fma(row[k], sm.xv[wave][k], xh);
+    }
+    const double n2 = wave_sum_f64(xh * xh);
+    const double u = (n2 > 0.0) ? xh * (8.0 / sqrt(n2)) : 0.0;
+    double lv = c[0];
+#pragma unroll
+    for (int k = 0; k < 7; ++k) lv = (u > th[k]) ? c[k + 1] : lv;
+    acc += fabs(u - lv);
+    if (rot) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");   // xv is rewritten next
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+  }
+  sm.red[t] = acc;
+  __syncthreads();
+  if (t == 0) {
+    double total = 0.0;
+    for (int i = 0; i < 256; ++i) total += sm.red[i];
+    const double mean = total / ((double)ncal * kDim);
+    ebar_out[(int64_t)head * stride] = asc ? (float)mean : __int_as_float(0x7FC00000);
+  }
+}
+
+hipError_t launch_calibrate_ebar(const float* x, int nheads, int ncal, const float* pi, const float* lut,
+                                 float* ebar_out, int stride, hipStream_t st) {
+  hipLaunchKernelGGL(calibrate_ebar_kernel, dim3(nheads), dim3(256), 0, st, x, ncal, pi, lut, ebar_out,
+                     stride);
+  return hipGetLastError();
+}
+
 }  // namespace tq

@@ -42,8 +42,6 @@
 //             sign bits.
 // Work items are dealt so that all splits of a unit land on one XCD (blocks
 // go to the 8 XCDs round-robin), where Pi stays in that XCD's L2.
-#include <stdlib.h>
-
 #include "tq_append.hpp"
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
@@ -52,7 +50,6 @@ namespace tq {
 
 constexpr float kLazyRescale = 8.0f;   // log2 headroom before the max is raised
 constexpr int kXcds = 8;
-constexpr int kSpin = 1 << 22;     // bound of a wait on an LDS count (never reached)
 
 // Block barrier that orders LDS only. __syncthreads() also waits for every
 // outstanding global load of the wave (its release fence covers global
@@ -295,6 +292,10 @@ struct Lut8 {
     const float2 a = pair_f2(w[0]), b = pair_f2(w[1]), c = pair_f2(w[2]), d = pair_f2(w[3]);
     return Lut8{a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
   }
+  // strictly ascending (false for any NaN level)
+  __device__ __forceinline__ bool ascending() const {
+    return (c0 < c1) & (c1 < c2) & (c2 < c3) & (c3 < c4) & (c4 < c5) & (c5 < c6) & (c6 < c7);
+  }
   __device__ __forceinline__ float pick(int i) const {
     const bool b0 = (i & 1) != 0, b1 = (i & 2) != 0, b2 = (i & 4) != 0;
     const float p01 = b0 ? c1 : c0, p23 = b0 ? c3 : c2, p45 = b0 ? c5 : c4, p67 = b0 ? c7 : c6;
@@ -354,6 +355,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   __shared__ __attribute__((aligned(16))) float s_vec[7][kDim];
   __shared__ uint32_t s_new[2 + 8 + kDim];                           // the appended token's codes
   __shared__ int s_ready;                                            // appends done
+  __shared__ int s_fail;                                             // a step's wait gave up
   __shared__ float s_vtab[16];
   __shared__ float s_wm[WAVES], s_wl[WAVES];
   __shared__ int s_last;
@@ -456,8 +458,12 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   const Lut8 ck = Lut8::of(kw), cvl = Lut8::of(vw);
   const float ebar_k = paper ? ebar_raw : 0.0f;
   const int n = len + len_add;             // tokens attended (the step's new one included)
+  // a unit whose sequence range or query position is out of bounds, or
+  // whose K or V table is not strictly ascending, is not appended to and
+  // gets NaN output
+  const bool asc = ck.ascending() && cvl.ascending();
   const bool valid = (n >= 0) & (n <= a.max_len) & (s0 >= 0) & ((s0 & 63) == 0) &
-                     (s0 + n <= a.slots) & (qp >= 0) & (qp < rope_positions);
+                     (s0 + n <= a.slots) & (qp >= 0) & (qp < rope_positions) & asc;
   if (!valid || n == 0) {
     if (split == 0 && t < kDim) store_out(a, unit, t, valid ? 0.0f : __int_as_float(0x7FC00000));
     __builtin_amdgcn_s_waitcnt(0);         // no copy into LDS outlives the block
@@ -482,7 +488,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 
   // Pi and S have arrived (every wave waits for its own copies, then the
   // barrier).
-  if (t == 0) s_ready = 0;
+  if (t == 0) { s_ready = 0; s_fail = 0; }
   __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0)
   lds_barrier();
 
@@ -621,11 +627,18 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
       const int tt = tb + d * WAVES;
       if (tt >= tile_end) break;
       if (app && tt == tnew) {
-        for (int i = 0; i < kSpin; ++i) {
-          if (__hip_atomic_load(&s_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= 2) break;
+        // bounded wait for the two appends; if it gives up, the unit's
+        // output is marked NaN (s_fail) instead of scoring stale codes
+        bool got = false;
+        for (int i = 0; i < a.wait_limit; ++i) {
+          if (__hip_atomic_load(&s_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= 2) {
+            got = true;
+            break;
+          }
           __builtin_amdgcn_s_sleep(1);
         }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+        if (!got && lane == 0) s_fail = 1;
         patch_new_token(buf[d], s_new, rnew, lane);
       }
       const TileRegs& cur = buf[d];
@@ -710,6 +723,9 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
       O += s_wo[w * kDim + t] * f;
       if (VQJL) SG += s_wsg[w * kDim + t] * f;
     }
+    // a failed step wait poisons the split's sum of weights: the merged
+    // output of the unit is then NaN
+    if (s_fail) L = __int_as_float(0x7FC00000);
   }
 
   if (participants > 1) {
@@ -776,8 +792,23 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
         }
       }
       L = wave_sum_uniform(Ll);
+      // Leave the workspace as it was found, all zero: each lane clears what
+      // it read (o and s of every partial at its dimension, and the (m, l)
+      // of the partials it loaded), after reading it (same addresses, so in
+      // program order).
+      for (int p = 0; p < participants; ++p) {
+        float* pq = a.partials + ((int64_t)unit * a.nsplit + p) * kPartialFloats;
+        pq[4 + lane] = 0.0f;
+        if (VQJL) pq[4 + kDim + lane] = 0.0f;
+      }
+      for (int p0 = 0; p0 < participants; p0 += 64) {
+        if (p0 + lane < participants) {
+          float* pp = a.partials + ((int64_t)unit * a.nsplit + p0 + lane) * kPartialFloats;
+          pp[0] = 0.0f;
+          pp[1] = 0.0f;
+        }
+      }
     }
-    // leave the workspace zeroed for the next call
     if (t == 0) __hip_atomic_store(a.counters + unit, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
 
@@ -834,24 +865,16 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 
 void decode_plan(int units, int max_len, int* waves, int* nsplit, int* split_tiles) {
   const int ntiles = max_len > 0 ? (max_len + 63) / 64 : 1;
-  int w = ntiles >= 12 ? 8 : 4;
-  const char* ew = getenv("TQ_DECODE_WAVES");
-  if (ew && (atoi(ew) == 4 || atoi(ew) == 8)) w = atoi(ew);
-  int st;
-  const char* env = getenv("TQ_DECODE_SPLIT_TILES");
-  if (env && atoi(env) > 0) {
-    st = atoi(env);
-  } else {
-    // One block per unit when there are enough units to occupy every CU
-    // (a cross-block merge costs more than it balances); otherwise split the
-    // tiles so that each wave still gets at least one tile.
-    const int target_blocks = 256;
-    int ns = (target_blocks + units - 1) / units;
-    const int max_ns = (ntiles + w - 1) / w;
-    if (ns > max_ns) ns = max_ns;
-    if (ns < 1) ns = 1;
-    st = (ntiles + ns - 1) / ns;
-  }
+  const int w = ntiles >= 12 ? 8 : 4;
+  // One block per unit when there are enough units to occupy every CU
+  // (a cross-block merge costs more than it balances); otherwise split the
+  // tiles so that each wave still gets at least one tile.
+  const int target_blocks = 256;
+  int ns = (target_blocks + units - 1) / units;
+  const int max_ns = (ntiles + w - 1) / w;
+  if (ns > max_ns) ns = max_ns;
+  if (ns < 1) ns = 1;
+  int st = (ntiles + ns - 1) / ns;
   if (st > ntiles) st = ntiles;
   *waves = w;
   *split_tiles = st;

@@ -1,6 +1,6 @@
 // Dequantize the packed cache into fp16 key and value rows: the first step of
 // a "dequantize first, then attend" path, the comparison the paper makes for
-// its fused kernel (Sec. 5.4, Table 6). The rows are what the fused decode
+// its fused kernel (Sec. 5.3, Table 6). The rows are what the fused decode
 // reconstructs in registers (Sec. 3.1 decode, Sec. 3.4):
 //   k~_j = (n_k/8) (c_K[idx_j] + alpha g_k S^T (2 s_j - 1))
 //          (per-element form: ebar_K (2 s_j - 1) in place of alpha g_k S^T (2 s_j - 1))
@@ -78,6 +78,9 @@ __global__ __launch_bounds__(256) void dequant_kernel(DequantArgs a) {
   const int len = a.seq_len[b];
   const int64_t s0 = a.seq_slot0[b];
   if (len <= 0 || len > a.max_len || s0 < 0 || (s0 & 63) != 0 || s0 + len > a.slots) return;
+  // a (layer, head) whose K or V table is not strictly ascending is skipped
+  if (!levels_ascending(load_levels(a.lut_k + lh * 8)) || !levels_ascending(load_levels(a.lut_v + lh * 8)))
+    return;
   const int ntiles = (len + 63) >> 6;
   const int tile_first = blockIdx.x * kTilesPerBlock;
   if (tile_first >= ntiles) return;   // block-uniform, before any barrier

@@ -95,6 +95,13 @@ __device__ __forceinline__ Levels load_levels(const float* lut) {
   return L;
 }
 
+// Strictly ascending levels (false for any NaN level). Kernels skip a
+// (layer, head) whose table fails this: the midpoint rule assumes it.
+__device__ __forceinline__ bool levels_ascending(const Levels& L) {
+  return (L.c0 < L.c1) & (L.c1 < L.c2) & (L.c2 < L.c3) & (L.c3 < L.c4) & (L.c4 < L.c5) &
+         (L.c5 < L.c6) & (L.c6 < L.c7);
+}
+
 // Nearest level of u by the midpoints (ties go to the lower level): returns
 // the level, its index in *idx.
 // The levels are passed as separate values, which callers pin in registers

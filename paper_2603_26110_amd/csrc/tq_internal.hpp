@@ -62,7 +62,11 @@ struct DecodeArgs {
   const void* v_new;
   int append;
   int len_add;
+  int wait_limit;          // polls of a decode step's wait for its appends before giving up
 };
+
+// Default bound of that wait (never reached: the appends wait on nothing).
+constexpr int kDefaultWaitLimit = 1 << 22;
 
 constexpr int kPartialFloats = 2 * 64 + 4;   // m, l, pad, pad, o[64], s[64]
 
@@ -96,6 +100,8 @@ struct LutInit {
 };
 hipError_t launch_calibrate_lut(const float* x, int nheads, int ncal, const float* pi, const float* init,
                                 int max_iter, double tol, float* lut_out, hipStream_t st);
+hipError_t launch_calibrate_ebar(const float* x, int nheads, int ncal, const float* pi, const float* lut,
+                                 float* ebar_out, int stride, hipStream_t st);
 hipError_t launch_calibrate(const float* x, int nheads, int ncal, float* pi_out,
                             float* sing_out, hipStream_t st);
 

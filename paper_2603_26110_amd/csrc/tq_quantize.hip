@@ -371,6 +371,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
 
   const int j0 = blockIdx.x * 256 + wave * kTile;
   if (j0 >= a.T) return;                  // wave-uniform; no barrier follows
+  // a (layer, head) whose K or V table is not strictly ascending is not written
+  if (!levels_ascending(Lk) || !levels_ascending(Lv)) return;
   const int j = j0 + lane;
   const int64_t sbase = a.slot0[b];
   const int pbase = a.pos0[b];
@@ -508,13 +510,16 @@ __global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, uint
   // ---- loads that do not depend on the slot, issued first
   float x = load_in(is_v ? a.v : a.k, row + i, F16);
   const Levels L = load_levels((is_v ? a.lut_v : a.lut_k) + lh * 8);
+  const Levels Lo = load_levels((is_v ? a.lut_k : a.lut_v) + lh * 8);
   MatrixSlice pi_sl, s_sl;
   if (any_rotate) load_slice(a.pi + lh * kDim * kDim, pi_sl, threadIdx.x);
   if (any_proj) load_slice(a.qjl_s, s_sl, threadIdx.x);
   const int64_t slot = a.slot0[b] + j;
   const int pos = a.pos0[b] + (int)j;
-  // block-uniform exits (before any barrier)
+  // block-uniform exits (before any barrier); a (layer, head) whose K or V
+  // table is not strictly ascending is not written
   if (slot < 0 || slot >= a.slots) return;
+  if (!levels_ascending(L) || !levels_ascending(Lo)) return;
   if (!rotated && (pos < 0 || pos >= a.rope_positions)) return;
   const bool half = (a.flags & kRopeHalf) != 0;
   float2 cs = make_float2(1.0f, 0.0f);

@@ -14,8 +14,8 @@ Calibration follows the paper's recipe (Sec. 3.2, Sec. 3.3): the head-wise
 rotation is the SVD basis of calibration keys (tq_calibrate_rotation), the
 tables are the 1-D Lloyd iteration on the normalized rotated coordinates of
 calibration keys and values (tq_calibrate_lut), and the per-head mean
-residual magnitudes of the per-element sign correction are measured on the
-same calibration vectors. Calibration vectors are drawn from the same
+residual magnitudes of the per-element sign correction come from
+tq_calibrate_ebar on the same calibration vectors. Calibration vectors are drawn from the same
 distributions at seeded positions.
 
     python -m paper_2603_26110_amd.quality [--heads 20] [--tokens 1024] [--calib 4096]
@@ -55,23 +55,11 @@ def exact_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, qpos: int) -> n
     return np.einsum("ht,htd->hd", w, np.transpose(v, (1, 0, 2)).astype(np.float64))
 
 
-def _mean_abs_residual(x: torch.Tensor, pi: torch.Tensor | None, lut: torch.Tensor) -> torch.Tensor:
-    """Per head, the mean |u_i - c(u_i)| over the calibration coordinates
-    u = 8 x^ / |x^| (x^ = pi x), c(u) the nearest level: the per-head constant
-    of the per-element sign correction (paper form). x: [H][n][64]."""
-    xh = x if pi is None else torch.bmm(x, pi.transpose(1, 2).contiguous())
-    nrm = torch.linalg.vector_norm(xh, dim=2, keepdim=True)
-    u = torch.where(nrm > 0, xh * (8.0 / nrm.clamp_min(1e-30)), torch.zeros_like(xh))
-    t = 0.5 * (lut[:, :-1] + lut[:, 1:])                           # [H][7]
-    idx = (u[..., None] > t[:, None, None, :]).sum(-1)             # [H][n][64]
-    c = torch.gather(lut[:, None, :].expand(-1, idx.shape[1], -1), 2, idx)
-    return (u - c).abs().mean(dim=(1, 2))
-
-
-def run(heads: int = 20, tokens: int = 1024, calib: int = 4096, seed: int = 20261) -> list[dict]:
-    import paper_2603_26110_amd as tq
-
-    dev = torch.device("cuda")
+def inputs(heads: int = 20, tokens: int = 1024, calib: int = 4096, seed: int = 20261) -> dict:
+    """The seeded raw inputs of the ablation (numpy): keys and values
+    [1][1][T][H][64] and the query [1][1][H][64] (fp16 values), S, a random
+    rotation per head, and the calibration sets: post-RoPE keys and values
+    [H][calib][64] (fp32). Also the fp64 exact-attention reference [H][64]."""
     g = synth.rng(seed)
     H, T = heads, tokens
     ch = synth.outlier_channels(g, 1, H)
@@ -80,66 +68,101 @@ def run(heads: int = 20, tokens: int = 1024, calib: int = 4096, seed: int = 2026
     q = synth.as_io(synth.queries(g, 1, 1, H), "f16")                 # [1][1][H][64]
     S = synth.qjl_matrix(g)
     pi_qr = synth.rotations(g, 1, H)[0]                                # [H][64][64]
-    # calibration keys (RoPE'd at seeded positions) and values, same distributions
     kc = synth.keys(g, 1, 1, calib, H, ch)[0, 0].astype(np.float32)   # [n][H][64]
     vc = synth.values(g, 1, 1, calib, H)[0, 0].astype(np.float32)
     pc = synth.calibration_positions(g, calib, T)
     kc_r = _rope(np.transpose(kc, (1, 0, 2)), pc).astype(np.float32)  # [H][n][64]
     vc_h = np.ascontiguousarray(np.transpose(vc, (1, 0, 2)))
     ref = exact_attention(q[0, 0].astype(np.float64), k[0, 0], v[0, 0], T - 1)
+    return {"H": H, "T": T, "k": k, "v": v, "q": q, "S": S, "pi_qr": pi_qr, "kc": kc_r, "vc": vc_h, "ref": ref}
 
-    t_ = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
-    kc_d, vc_d = t_(kc_r), t_(vc_h)
-    pi_svd, _ = tq.calibrate_rotation(kc_d)
-    eye = torch.eye(64, dtype=torch.float32, device=dev).expand(H, 64, 64).contiguous()
-    gauss = torch.from_numpy(synth.GAUSS_LEVELS_MAX1960).to(dev).expand(H, 8).contiguous()
-    cs = tq.rope_table(T + 64)
-    S_d, S0 = t_(S), torch.zeros((64, 64), dtype=torch.float32, device=dev)
-    k_d, v_d, q_d = t_(k), t_(v), t_(q)
 
-    def tables(pi):
-        return tq.calibrate_lut(kc_d, pi), tq.calibrate_lut(vc_d, pi)
+# Variant names, in the order of the table (the Table 7 ablations).
+VARIANTS = [
+    "no rotation (Pi = I), Gaussian tables, QJL",
+    "random-QR Pi, Gaussian tables, QJL",
+    "random-QR Pi, Gaussian tables, no QJL (S = 0)",
+    "random-QR Pi, Gaussian tables, per-element signs + ebar (paper QJL)",
+    "random-QR Pi, one calibrated table for K and V, QJL",
+    "random-QR Pi, calibrated K and V tables, QJL",
+    "SVD Pi, Gaussian tables, QJL",
+    "SVD Pi, calibrated K and V tables, QJL",
+    "SVD Pi, calibrated K and V tables, no QJL (S = 0)",
+]
 
-    def measure(pi, lut_k, lut_v, s_mat, flags, ebar=None):
-        params = tq.Params(1, H, cs, io_dtype=torch.float16, flags=flags | tq.OUT_FP32)
-        cache = tq.Cache(1, H, (T + 63) // 64 * 64)
-        i32 = lambda x: torch.tensor([x], dtype=torch.int32, device=dev)
-        i64 = lambda x: torch.tensor([x], dtype=torch.int64, device=dev)
-        lk, lv = lut_k.reshape(1, H, 8).contiguous(), lut_v.reshape(1, H, 8).contiguous()
-        pi1 = pi.reshape(1, H, 64, 64).contiguous()
-        eb = None if ebar is None else ebar.reshape(1, H, 2).contiguous()
-        tq.quantize_pack(params, cache, k_d, v_d, i32(0), i64(0), pi1, lk, lv, s_mat, eb)
-        out = tq.decode_attend(params, cache, q_d, i32(T - 1), i64(0), i32(T), T, pi1, lk, lv, s_mat, eb)
-        o = out.double().cpu().numpy()[0, 0]
-        cos = (o * ref).sum(1) / (np.linalg.norm(o, axis=1) * np.linalg.norm(ref, axis=1))
-        rel = np.linalg.norm(o - ref, axis=1) / np.linalg.norm(ref, axis=1)
-        return {"cos_mean": float(cos.mean()), "cos_min": float(cos.min()), "rel_l2": float(rel.mean())}
 
-    pi_qr_d = t_(pi_qr)
-    lk_qr, lv_qr = tables(pi_qr_d)
-    lk_svd, lv_svd = tables(pi_svd)
-    shared_qr = tq.calibrate_lut(torch.cat([kc_d, vc_d], 1), pi_qr_d)
-    e_k = _mean_abs_residual(kc_d, pi_qr_d, gauss)
-    e_v = _mean_abs_residual(vc_d, pi_qr_d, gauss)
-    ebar = torch.stack([e_k, e_v], 1)
-
-    R = tq.V_ROTATE
-    variants = [
-        ("no rotation (Pi = I), Gaussian tables, QJL", eye, gauss, gauss, S_d, R, None),
-        ("random-QR Pi, Gaussian tables, QJL", pi_qr_d, gauss, gauss, S_d, R, None),
-        ("random-QR Pi, Gaussian tables, no QJL (S = 0)", pi_qr_d, gauss, gauss, S0, R, None),
-        ("random-QR Pi, Gaussian tables, per-element signs + ebar (paper QJL)", pi_qr_d, gauss, gauss, S_d,
-         R | tq.QJL_PAPER, ebar),
-        ("random-QR Pi, one calibrated table for K and V, QJL", pi_qr_d, shared_qr, shared_qr, S_d, R, None),
-        ("random-QR Pi, calibrated K and V tables, QJL", pi_qr_d, lk_qr, lv_qr, S_d, R, None),
-        ("SVD Pi, Gaussian tables, QJL", pi_svd, gauss, gauss, S_d, R, None),
-        ("SVD Pi, calibrated K and V tables, QJL", pi_svd, lk_svd, lv_svd, S_d, R, None),
-        ("SVD Pi, calibrated K and V tables, no QJL (S = 0)", pi_svd, lk_svd, lv_svd, S0, R, None),
+def variant_parameters(inp: dict, rotation, table, ebar) -> list[dict]:
+    """Pi, tables, S, flags and ebar of every variant (numpy, fp32), from the
+    calibration callables rotation(x [H][n][64]) -> Pi [H][64][64],
+    table(x, pi) -> [H][8] and ebar(x, pi, lut) -> [H] (the library's, or
+    any other implementation of Sec. 3.2-3.4)."""
+    H = inp["H"]
+    eye = np.broadcast_to(np.eye(64, dtype=np.float32), (H, 64, 64)).copy()
+    gauss = np.broadcast_to(synth.GAUSS_LEVELS_MAX1960, (H, 8)).copy()
+    S, S0 = inp["S"], np.zeros((64, 64), np.float32)
+    pi_qr = inp["pi_qr"]
+    pi_svd = rotation(inp["kc"])
+    lk_qr, lv_qr = table(inp["kc"], pi_qr), table(inp["vc"], pi_qr)
+    lk_svd, lv_svd = table(inp["kc"], pi_svd), table(inp["vc"], pi_svd)
+    shared_qr = table(np.concatenate([inp["kc"], inp["vc"]], 1), pi_qr)
+    eb = np.stack([ebar(inp["kc"], pi_qr, gauss), ebar(inp["vc"], pi_qr, gauss)], 1).astype(np.float32)
+    R = 1   # V_ROTATE
+    rows = [
+        (eye, gauss, gauss, S, R, None), (pi_qr, gauss, gauss, S, R, None), (pi_qr, gauss, gauss, S0, R, None),
+        (pi_qr, gauss, gauss, S, R | 4, eb), (pi_qr, shared_qr, shared_qr, S, R, None),
+        (pi_qr, lk_qr, lv_qr, S, R, None), (pi_svd, gauss, gauss, S, R, None),
+        (pi_svd, lk_svd, lv_svd, S, R, None), (pi_svd, lk_svd, lv_svd, S0, R, None),
     ]
+    return [{"variant": name, "pi": np.ascontiguousarray(p, np.float32), "lut_k": np.ascontiguousarray(a, np.float32),
+             "lut_v": np.ascontiguousarray(b, np.float32), "S": np.ascontiguousarray(sm, np.float32), "flags": f,
+             "ebar": e} for name, (p, a, b, sm, f, e) in zip(VARIANTS, rows)]
+
+
+def decode_variant(inp: dict, var: dict) -> np.ndarray:
+    """tq_quantize_pack of the T tokens, then tq_decode_attend of the query at
+    position T - 1 (fp32 output): [H][64]."""
+    import paper_2603_26110_amd as tq
+    dev = torch.device("cuda")
+    H, T = inp["H"], inp["T"]
+    t_ = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    cs = tq.rope_table(T + 64)
+    params = tq.Params(1, H, cs, io_dtype=torch.float16, flags=var["flags"] | tq.OUT_FP32)
+    cache = tq.Cache(1, H, (T + 63) // 64 * 64)
+    i32 = lambda x: torch.tensor([x], dtype=torch.int32, device=dev)
+    i64 = lambda x: torch.tensor([x], dtype=torch.int64, device=dev)
+    lk, lv = t_(var["lut_k"].reshape(1, H, 8)), t_(var["lut_v"].reshape(1, H, 8))
+    pi1 = t_(var["pi"].reshape(1, H, 64, 64))
+    s_mat = t_(var["S"])
+    eb = None if var["ebar"] is None else t_(var["ebar"].reshape(1, H, 2))
+    tq.quantize_pack(params, cache, t_(inp["k"]), t_(inp["v"]), i32(0), i64(0), pi1, lk, lv, s_mat, eb)
+    out = tq.decode_attend(params, cache, t_(inp["q"]), i32(T - 1), i64(0), i32(T), T, pi1, lk, lv, s_mat, eb)
+    return out.double().cpu().numpy()[0, 0]
+
+
+def metrics(o: np.ndarray, ref: np.ndarray) -> dict:
+    cos = (o * ref).sum(1) / (np.linalg.norm(o, axis=1) * np.linalg.norm(ref, axis=1))
+    rel = np.linalg.norm(o - ref, axis=1) / np.linalg.norm(ref, axis=1)
+    return {"cos_mean": float(cos.mean()), "cos_min": float(cos.min()), "rel_l2": float(rel.mean())}
+
+
+def library_calibration():
+    """The three calibration callables of variant_parameters, by the library
+    (tq_calibrate_rotation, tq_calibrate_lut, tq_calibrate_ebar)."""
+    import paper_2603_26110_amd as tq
+    dev = torch.device("cuda")
+    t_ = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+    rotation = lambda x: tq.calibrate_rotation(t_(x))[0].cpu().numpy()
+    table = lambda x, pi: tq.calibrate_lut(t_(x), t_(pi)).cpu().numpy()
+    ebar = lambda x, pi, lut: tq.calibrate_ebar(t_(x), t_(lut), t_(pi)).cpu().numpy()
+    return rotation, table, ebar
+
+
+def run(heads: int = 20, tokens: int = 1024, calib: int = 4096, seed: int = 20261) -> list[dict]:
+    inp = inputs(heads, tokens, calib, seed)
     rows = []
-    for name, pi, lk, lv, s_mat, flags, eb in variants:
-        r = measure(pi, lk, lv, s_mat, flags, eb)
-        r["variant"] = name
+    for var in variant_parameters(inp, *library_calibration()):
+        r = metrics(decode_variant(inp, var), inp["ref"])
+        r["variant"] = var["variant"]
         rows.append(r)
     return rows
 

@@ -202,3 +202,55 @@ def assert_agree_up_to_threshold_rounding(case, got, ref, B, T, H, tokens=None):
     # a sign bit follows the residual: it may flip with a code, or where its
     # projection is within rounding of zero
     assert sign_diff <= 64 * code_diff + 1e-4 * total
+
+
+def unpack_planes(k_region: np.ndarray, v_region: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    """All nibbles (idx | sign << 3) of one (layer, head) region, [slots][64]
+    for keys and values, decoded with NumPy from the documented layout (see
+    unpack_slot)."""
+    kw = np.ascontiguousarray(k_region).view(np.uint32).reshape(-1, 2, 64, 4)      # [tile][c][r][wi]
+    nt = kw.shape[0]
+    j = np.arange(8, dtype=np.uint32)
+    # key word w = 4c + wi of slot (tile, r): dims 8w + j
+    kw = kw.transpose(0, 2, 1, 3).reshape(nt, 64, 8)                                # [tile][r][w]
+    idx = (kw[..., None] >> (3 * j)) & 7
+    sgn = (kw[..., None] >> (24 + j)) & 1
+    knib = (idx | (sgn << 3)).reshape(nt * 64, 64).astype(np.uint8)
+    vw = np.ascontiguousarray(v_region).view(np.uint32).reshape(-1, 2, 64, 4)       # [tile][c][i][wi]
+    nib = (vw[..., None] >> (4 * j)) & 15                                           # [tile][c][i][wi][n]
+    # slot r = 32c + 8wi + n of dimension i
+    vnib = nib.transpose(0, 1, 3, 4, 2).reshape(nt * 64, 64).astype(np.uint8)
+    return knib, vnib
+
+
+def assert_region_agrees(got_k, got_v, got_s, ref_k, ref_v, ref_s, n, rotated_of):
+    """The first n slots of one (layer, head) region written by the GPU and by
+    the oracle from the same raw tokens: fp16 norms within one ulp; codes
+    equal, or one level apart where the oracle's fp64 coordinate lies within
+    rounding of a threshold (rotated_of(slot, is_key) -> (x^ fp32, table));
+    sign bits differ only with a code or within rounding of zero.
+    Returns (codes compared, codes differing)."""
+    gs = got_s.reshape(-1, 4)[:n].view(np.float16).astype(np.float64)
+    os_ = ref_s.reshape(-1, 4)[:n].view(np.float16).astype(np.float64)
+    for col in (0, 2):
+        assert np.all(np.abs(gs[:, col] - os_[:, col]) <= fp16_ulp(os_[:, col]) + 1e-12), col
+    gk, gv = unpack_planes(got_k, got_v)
+    rk, rv = unpack_planes(ref_k, ref_v)
+    total = diff = sdiff = 0
+    for is_key, g_, r_ in ((True, gk[:n], rk[:n]), (False, gv[:n], rv[:n])):
+        total += g_.size
+        bad = (g_ & 7) != (r_ & 7)
+        sdiff += int(((g_ >> 3) != (r_ >> 3)).sum())
+        for s in np.nonzero(bad.any(axis=1))[0]:
+            xh, lut = rotated_of(int(s), is_key)
+            xd = xh.astype(np.float64)
+            u = xd * 8.0 / np.linalg.norm(xd)
+            t = 0.5 * (lut[:-1].astype(np.float64) + lut[1:])
+            dist = np.min(np.abs(u[:, None] - t[None, :]), axis=1)
+            b = bad[s]
+            assert np.all(dist[b] < 1e-4), (int(s), is_key, dist[b])
+            assert np.all(np.abs((g_[s][b] & 7).astype(int) - (r_[s][b] & 7)) == 1)
+        diff += int(bad.sum())
+    assert diff <= 1e-3 * total
+    assert sdiff <= 64 * diff + 1e-4 * total
+    return total, diff

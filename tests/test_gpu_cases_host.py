@@ -34,3 +34,19 @@ def test_device_bytes_regions():
             np.testing.assert_array_equal(db.region("k", l, h), oc.region("k", l, h))
             np.testing.assert_array_equal(db.region("v", l, h), oc.region("v", l, h))
             np.testing.assert_array_equal(db.scalars(l, h), oc.scalars(l, h))
+
+
+def test_unpack_planes_matches_the_per_slot_unpackers():
+    # the vectorized reader of whole regions against the per-slot reader of
+    # the tests and the oracle's own unpacker, on random bytes
+    from gpu_cases import unpack_planes, unpack_slot
+    g = np.random.default_rng(3)
+    reg_k = g.integers(0, 256, 3 * 2048, dtype=np.uint8)
+    reg_v = g.integers(0, 256, 3 * 2048, dtype=np.uint8)
+    kn, vn = unpack_planes(reg_k, reg_v)
+    assert kn.shape == (192, 64) and vn.shape == (192, 64)
+    for s in range(0, 192, 7):
+        assert np.array_equal(kn[s], unpack_slot(reg_k, s, "k"))
+        assert np.array_equal(vn[s], unpack_slot(reg_v, s, "v"))
+        assert np.array_equal(kn[s], oracle.unpack_slot(reg_k, s, "k"))
+        assert np.array_equal(vn[s], oracle.unpack_slot(reg_v, s, "v"))

@@ -8,9 +8,11 @@ kernel reads the whole packed cache).
                           tile-aligned packed offsets
   ESM-2 3B shape          36 layers x 40 heads, batch 16, 8192 cached tokens
 
-For a sample of (layer, sequence, head) units the oracle quantizes that
-unit's raw tokens (the cached ones and the new one) into a cache of its own
-and decodes there in fp64: 2e-3 on the fp32 output and max(2e-3, 1 fp16 ulp)
+At the ESM-2 650M shape every unit is compared: the oracle quantizes all the
+raw tokens into a cache of its own and decodes every unit there in fp64. At
+the ragged and 3B shapes, for a sample of (layer, sequence, head) units the
+oracle quantizes that unit's raw tokens (the cached ones and the new one)
+into a cache of its own and decodes there in fp64: 2e-3 on the fp32 output and max(2e-3, 1 fp16 ulp)
 on the fp16 output. The GPU's codes of sampled tokens, including the appended
 one, are checked against the oracle's quantizer of the same inputs: equal, or
 one level apart where the rotated coordinate lies within rounding of a
@@ -21,7 +23,7 @@ import pytest
 import torch
 
 import paper_2603_26110_amd as tq
-from gpu_cases import DeviceBytes, GAUSS_LUT, fp16_ulp, unpack_slot
+from gpu_cases import DeviceBytes, GAUSS_LUT, assert_region_agrees, device_bytes, fp16_ulp, unpack_slot
 from oracle import oracle
 from paper_2603_26110_amd import synth
 
@@ -140,7 +142,8 @@ def _sample_units(g, L, B, H, n):
 
 
 def test_full_650m_33layer_step():
-    # the bench's workload and inputs (same seed and draw order)
+    # the bench's workload and inputs (same seed and draw order); every one of
+    # the 660 (layer, head) units is compared with the oracle
     wl = synth.WORKLOADS["esm2-650m-33layer-seq1024"]
     L, H, T = wl.layers, wl.heads, wl.seq
     g = synth.rng(wl.seed)
@@ -164,20 +167,38 @@ def test_full_650m_33layer_step():
     out16, out32 = _step_both_outputs(params, cache, t_(q), t_(k[:, :, T]), t_(v[:, :, T]), [T], [0], [T],
                                       T + 1, pi_d, lk_d, lv_d, S_d)
     assert np.all(np.isfinite(out32))
-    units = _sample_units(synth.rng(1), L, 1, H, 24)
-    raw = {(l, b, h): (k[l, b, :T + 1, h].astype(np.float32), v[l, b, :T + 1, h].astype(np.float32))
-           for (l, b, h) in units}
-    _check_units(cache, units, raw, out16, out32, q.astype(np.float32), [T], [0], [T + 1], pi, lut_k, lut_v,
-                 S, tq.V_ROTATE, cs_host)
-    samples = [(l, h, j, j, k[l, 0, j, h], v[l, 0, j, h])
-               for (l, _, h) in units[:8] for j in (0, 63, 64, 777, T - 1, T)]
-    _check_codes(cache, samples, cs_host, pi, lut_k, lut_v, S, tq.V_ROTATE)
+    # the oracle quantizes the same T + 1 raw tokens of every unit (the T
+    # prefilled and the appended one) into a cache of its own and decodes
+    # every unit there in fp64
+    oc = oracle.Cache(L, H, slots)
+    oracle.quantize_pack(oc, tq.V_ROTATE, cs_host, k.astype(np.float32), v.astype(np.float32), [0], [0], pi,
+                         lut_k, lut_v, S)
+    ref = oracle.decode(oc, tq.V_ROTATE, cs_host, q.astype(np.float32), [T], [0], [T + 1], pi, lut_k, lut_v, S)
+    err = np.abs(out32.astype(np.float64) - ref)
+    assert np.max(err) <= TOL, np.unravel_index(np.argmax(err), err.shape)
+    r16 = ref.astype(np.float16).astype(np.float64)
+    assert np.all(np.abs(out16.astype(np.float64) - r16) <= np.maximum(TOL, fp16_ulp(r16)))
+    # every unit's codes and norms, the appended token's included
+    got = device_bytes(cache)
+    total = diff = 0
+    for l in range(L):
+        for h in range(H):
+            def rotated_of(s, is_key, l=l, h=h):
+                x = (k if is_key else v)[l, 0, s, h].astype(np.float32)
+                return (oracle.rotated_input(x, is_key, s, cs_host, pi[l, h]), (lut_k if is_key else lut_v)[l, h])
+            t, d = assert_region_agrees(got.region("k", l, h), got.region("v", l, h), got.scalars(l, h),
+                                        oc.region("k", l, h), oc.region("v", l, h), oc.scalars(l, h), T + 1,
+                                        rotated_of)
+            total += t
+            diff += d
+    print(f"650M step: max |err| {np.max(err):.3e} over 660 units; {diff} of {total} codes one level apart")
     # the two-step baseline at this size: fp32 softmax attention over the
     # dequantized fp16 rows reproduces the fused step's output to within the
     # bound the rows' fp16 rounding implies (see tests/test_gpu_dequant.py)
+    units = _sample_units(synth.rng(1), L, 1, H, 12)
     ko, vo = tq.dequantize(params, cache, _i64([0]), _i32([T + 1]), T + 1, lk_d, lv_d, S_d)
     torch.cuda.synchronize()
-    for (l, b, h) in units[:12]:
+    for (l, b, h) in units:
         kk = ko[l, b, h].float().cpu().numpy().astype(np.float64)
         vv = vo[l, b, h].float().cpu().numpy().astype(np.float64)
         qr = oracle.rope_apply(q[l, b, h].astype(np.float32), T, cs_host)

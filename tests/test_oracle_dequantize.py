@@ -1,5 +1,5 @@
 """Pins of the oracle's dequantize (the first step of a dequantize-then-attend
-path, the comparison of Sec. 5.4 / Table 6): textbook softmax attention over
+path, the comparison of Sec. 5.3 / Table 6): textbook softmax attention over
 the dequantized keys and values reproduces the oracle's decode, which is
 pinned on its own; the table term alone has the textbook distortion of the
 3-bit Lloyd-Max quantizer of N(0, 1); a hand-built slot gives the defined
