@@ -218,6 +218,27 @@ TQ_API tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache
                            void* out, void* workspace, size_t workspace_bytes,
                            void* stream);
 
+/* tq_decode_attend for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation and the same kernels, without a workspace
+ * argument. When the sizes need a split-K workspace
+ * (tq_decode_workspace_bytes > 0), the library uses a fixed device array of
+ * 262144 bytes that each GPU it runs on holds until the process ends, and
+ * first clears its counters with a small kernel on `stream`; sizes that
+ * would need more return TQ_ERR_CAPACITY before anything is launched. The
+ * call allocates nothing (no hipMalloc, no allocating library call).
+ * Every call on one GPU shares that GPU's array: calls that overlap on one
+ * GPU (other streams, other threads) race, so order them on one stream.
+ * `stream` must belong to the current device. Arguments and output as
+ * tq_decode_attend. */
+TQ_API tq_status tq_decode_attend_noalloc(const tq_params* params, const tq_cache* cache,
+                                          const void* q, int32_t B, int32_t layer0, int32_t nlayers,
+                                          const int32_t* q_pos, const int64_t* seq_slot0,
+                                          const int32_t* seq_len, int32_t max_len,
+                                          const float* pi, const float* lut_k, const float* lut_v,
+                                          const float* qjl_s, const float* ebar, void* out,
+                                          void* stream);
+
 /* One decode step (Sec. 3.1 decode steps: quantize-then-attend): for every
  * layer, sequence b and head, first append the new token exactly as
  * tq_quantize_pack with T = 1, pos0 = pos and slot0 = seq_slot0 + seq_len

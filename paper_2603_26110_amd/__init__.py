@@ -6,7 +6,7 @@ path runs in the library's HIP kernels. If the library is not built, calls
 raise ``RuntimeError`` (there is no fallback path).
 
 Entry points (same names as the C ABI without the ``tq_`` prefix):
-    rope_table, quantize_pack, decode_attend, decode_step, dequantize,
+    rope_table, quantize_pack, decode_attend, decode_attend_noalloc, decode_step, dequantize,
     decode_workspace_bytes, calibrate_rotation, calibrate_lut, calibrate_ebar, set_step_wait_limit,
     cache_bytes, last_error, version
 """
@@ -20,7 +20,7 @@ import torch
 
 __all__ = [
     "Params", "Cache", "TQError", "rope_table", "quantize_pack", "decode_attend", "decode_step", "dequantize",
-    "decode_workspace_bytes", "calibrate_rotation", "calibrate_lut", "calibrate_ebar", "set_step_wait_limit",
+    "decode_attend_noalloc", "decode_workspace_bytes", "calibrate_rotation", "calibrate_lut", "calibrate_ebar", "set_step_wait_limit",
     "cache_bytes", "last_error", "version",
     "V_ROTATE", "V_QJL", "QJL_PAPER", "ROPE_HALF", "INPUT_ROTATED", "OUT_FP32", "lib_path",
 ]
@@ -82,6 +82,8 @@ def _load():
     L.tq_calibrate_rotation.restype = i32
     L.tq_calibrate_ebar.argtypes = [P, i32, i32, P, P, P, i32, P]
     L.tq_calibrate_ebar.restype = i32
+    L.tq_decode_attend_noalloc.argtypes = [P, P, P, i32, i32, i32, P, P, P, i32, P, P, P, P, P, P, P]
+    L.tq_decode_attend_noalloc.restype = i32
     L.tq_set_step_wait_limit.argtypes = [i32]
     L.tq_set_step_wait_limit.restype = i32
     _lib = L
@@ -224,6 +226,36 @@ def decode_attend(params: Params, cache: Cache, q, q_pos, seq_slot0, seq_len, ma
                               _ptr(seq_slot0), _ptr(seq_len), int(max_len), _ptr(pi), _ptr(lut_k),
                               _ptr(lut_v), _ptr(qjl_s), _ptr(ebar), _ptr(out), _ptr(workspace),
                               wsz, _stream(q.device)))
+    return out
+
+
+def decode_attend_noalloc(params: Params, cache: Cache, q, q_pos, seq_slot0, seq_len, max_len: int,
+                          pi, lut_k, lut_v, qjl_s, ebar=None, layer0: int = 0, out=None) -> torch.Tensor:
+    """decode_attend without a workspace: the library's fixed split-K scratch
+    (see tq_decode_attend_noalloc). ``out`` should be passed where nothing may
+    be allocated."""
+    L = _load()
+    _dev(q, "q", params.io_dtype)
+    if q.dim() != 4 or q.shape[-1] != 64 or q.shape[2] != params.num_heads:
+        raise ValueError("q must be [nlayers][B][H][64]")
+    nl, B = q.shape[:2]
+    _dev(q_pos, "q_pos", torch.int32)
+    _dev(seq_slot0, "seq_slot0", torch.int64)
+    _dev(seq_len, "seq_len", torch.int32)
+    for name, t in (("pi", pi), ("lut_k", lut_k), ("lut_v", lut_v), ("qjl_s", qjl_s)):
+        _dev(t, name, torch.float32)
+    if ebar is not None:
+        _dev(ebar, "ebar", torch.float32)
+    out_dtype = torch.float32 if (params.flags & OUT_FP32 or params.io_dtype == torch.float32) \
+        else torch.float16
+    if out is None:
+        out = torch.empty(q.shape, dtype=out_dtype, device=q.device)
+    _dev(out, "out", out_dtype)
+    p = params.c()
+    c = cache.c()
+    _check(L.tq_decode_attend_noalloc(ctypes.byref(p), ctypes.byref(c), _ptr(q), B, layer0, nl, _ptr(q_pos),
+                                      _ptr(seq_slot0), _ptr(seq_len), int(max_len), _ptr(pi), _ptr(lut_k),
+                                      _ptr(lut_v), _ptr(qjl_s), _ptr(ebar), _ptr(out), _stream(q.device)))
     return out
 
 

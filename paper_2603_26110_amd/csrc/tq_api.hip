@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "../../include/turboesm.h"
 #include "tq_internal.hpp"
@@ -52,6 +53,25 @@ tq_status check_params(const tq_params* p, bool need_rope) {
     if (p->rope_positions <= 0) return fail(TQ_ERR_ARG, "rope_positions must be positive");
   }
   return ok();
+}
+
+// ---------------------------------------------------------------- scratch
+// The split-K workspace of tq_decode_attend_noalloc: a fixed device array.
+// Every GPU the library runs on holds its own copy until the process ends.
+// In host code `scratch` names a host-side stand-in, not device memory: host
+// code reaches the array only through the device address that
+// hipGetSymbolAddress returns for the current device, kept per device.
+constexpr size_t kScratchBytes = 256 * 1024;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxDevices] = {};
+
+// Clears n 32-bit words (a kernel rather than hipMemsetAsync, so that the
+// call can be captured into a HIP graph).
+__global__ void zero_words_kernel(uint32_t* p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
 }
 
 tq_status check_cache(const tq_cache* c) {
@@ -150,7 +170,7 @@ tq_status decode_common(const tq_params* params, const tq_cache* cache, const vo
                         const int64_t* seq_slot0, const int32_t* seq_len, int32_t max_len,
                         const float* pi, const float* lut_k, const float* lut_v, const float* qjl_s,
                         const float* ebar, void* out, void* workspace, size_t workspace_bytes,
-                        void* stream, bool step) {
+                        void* stream, bool step, bool clear_counters = false) {
   tq_status s = check_params(params, true);
   if (s != TQ_OK) return s;
   if ((s = check_cache(cache)) != TQ_OK) return s;
@@ -201,6 +221,14 @@ tq_status decode_common(const tq_params* params, const tq_cache* cache, const vo
     a.partials = (float*)ws;
     ws += align256((size_t)units * nsplit * tq::kPartialFloats * sizeof(float));
     a.counters = (uint32_t*)ws;
+    if (clear_counters) {
+      const int64_t n = units;
+      const int threads = 256;
+      const int blocks = (int)std::min<int64_t>((n + threads - 1) / threads, 1024);
+      hipLaunchKernelGGL(zero_words_kernel, dim3(blocks), dim3(threads), 0, (hipStream_t)stream, a.counters, n);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return fail(TQ_ERR_HIP, "counter clear launch: %s", hipGetErrorString(e));
+    }
   }
   return hip_status(tq::launch_decode(a, waves, (hipStream_t)stream),
                     step ? "tq_decode_step launch" : "tq_decode_attend launch");
@@ -219,6 +247,38 @@ tq_status tq_decode_attend(const tq_params* params, const tq_cache* cache, const
   return decode_common(params, cache, q, nullptr, nullptr, B, layer0, nlayers, q_pos, seq_slot0, seq_len,
                        max_len, pi, lut_k, lut_v, qjl_s, ebar, out, workspace, workspace_bytes, stream,
                        false);
+}
+
+tq_status tq_decode_attend_noalloc(const tq_params* params, const tq_cache* cache, const void* q, int32_t B,
+                                   int32_t layer0, int32_t nlayers, const int32_t* q_pos,
+                                   const int64_t* seq_slot0, const int32_t* seq_len, int32_t max_len,
+                                   const float* pi, const float* lut_k, const float* lut_v,
+                                   const float* qjl_s, const float* ebar, void* out, void* stream) {
+  const size_t need = tq_decode_workspace_bytes(params, B, nlayers, max_len);
+  void* ws = nullptr;
+  if (need > 0) {
+    if (need > kScratchBytes)
+      return fail(TQ_ERR_CAPACITY, "tq_decode_attend_noalloc: these sizes need %zu bytes of split-K workspace, "
+                  "more than its fixed %zu (use tq_decode_attend with a workspace)", need, kScratchBytes);
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail(TQ_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices) return fail(TQ_ERR_HIP, "device index %d out of range", dev);
+    {
+      std::lock_guard<std::mutex> lock(g_scratch_mu);
+      if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+          return fail(TQ_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+        g_scratch_dev[dev] = p;
+      }
+      ws = g_scratch_dev[dev];
+    }
+  }
+  return decode_common(params, cache, q, nullptr, nullptr, B, layer0, nlayers, q_pos, seq_slot0, seq_len,
+                       max_len, pi, lut_k, lut_v, qjl_s, ebar, out, ws, need > 0 ? kScratchBytes : 0, stream,
+                       false, true);
 }
 
 tq_status tq_decode_step(const tq_params* params, const tq_cache* cache, const void* q, const void* k,
