@@ -12,8 +12,19 @@ from the 256 MB Infinity Cache. The K timed steps are captured in one HIP
 graph and replayed once between two synchronizations; HIP events on the
 graph's stream give the average step duration for the roofline.
 
-Prints one JSON line (see the "value", "roofline" and "cpu_baseline" keys).
-    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+Besides the contract's keys ("value", "roofline", "cpu_baseline") the line
+carries: the median, p10 and p90 step time over further replays of the
+graph; the same step as 33 per-layer launches; a streaming read of the same
+bytes (tq_read_probe) as the size's read ceiling; the ragged batch of 64
+sequences and the ESM-2 3B shape ("configs": their own KV GB/s, roofline
+fraction, steps/s and an oracle sample timed with all threads and one); the
+GPU calibration time of the whole 650M model; the prefill, the
+dequantize-then-attend path and plain fp16 attention for context.
+
+Prints one JSON line.
+    python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra]
+    python bench.py --workload esm2-650m-ragged-b64     (one batched workload alone)
+    python bench.py --only prefill|dequant --steps K     (eager launches, for counters)
 """
 from __future__ import annotations
 
@@ -52,6 +63,13 @@ def parse():
     ap.add_argument("--eager", action="store_true",
                     help="launch the K timed steps one by one instead of as one HIP graph "
                          "(for counter collection)")
+    ap.add_argument("--only", choices=("prefill", "dequant"), default=None,
+                    help="run only K eager launches of the prefill quantizer or of the dequantize "
+                         "baseline on the headline shape (for counter collection)")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the ragged-batch and ESM-2 3B decode lines")
+    ap.add_argument("--replays", type=int, default=10,
+                    help="graph replays of the K steps behind the median and p10/p90 step times")
     return ap.parse_args()
 
 
@@ -84,7 +102,11 @@ def main():
         return
 
     wl = synth.WORKLOADS[args.workload]
-    assert wl.batch == 1 and wl.ragged is None, "the bench drives the batch-1 decode workloads"
+    if wl.batch != 1 or wl.ragged is not None:
+        # a batched workload on its own (the default line carries it as well)
+        print(json.dumps(workload_line(torch, tq, synth, wl.name, args.replays, args.cpu_seconds,
+                                       eager=args.eager, cpu=not args.no_cpu_baseline)))
+        return
     L, H, T = wl.layers, wl.heads, wl.seq
     n_ctx = T + 1                     # tokens attended per step (prefill + the new one)
     slots = ((n_ctx + 63) // 64) * 64
@@ -162,6 +184,10 @@ def main():
     assert torch.equal(eager_out, two_call_out), "decode_step differs from quantize_pack + decode_attend"
 
     K = args.steps
+    if args.only:
+        only_kernel(torch, tq, args.only, K, params, reps, base_cache, t_, k_all, v_all, T, n_ctx, L, H, slots,
+                    pi_d, lut_d, S_d, zero_i32, zero_i64)
+        return
     if args.eager:
         for s in range(K):
             (attend if args.decode_only else step)(s % R)
@@ -196,6 +222,8 @@ def main():
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / K
     step_ms = e0.elapsed_time(e1) / K
+    # spread over further replays of the same graph (not the timed region)
+    spread = replay_spread(torch, graph, stream, K, args.replays)
 
     # for comparison (not the headline): the same step as two calls, and the
     # attention call alone
@@ -262,6 +290,29 @@ def main():
         fp16_base["decode_attend_speedup_vs_sdpa"] = round(fp16_base["sdpa_ms"] / attend_ms, 2)
         fp16_base["decode_step_speedup_vs_sdpa"] = round(fp16_base["sdpa_ms"] / step_ms, 2)
 
+    per_layer = None
+    if not args.decode_only:
+        per_layer = per_layer_launches(torch, tq, params, reps, L, n_ctx, pos_new, zero_i64, cached, lut_d, S_d,
+                                       K, stream, kv_bytes)
+    probe = hbm_read_probe(torch, tq, alg_bytes, args.replica_bytes, K)
+    probe["decode_step_frac_of_probe"] = round(achieved / probe["gbs"], 4)
+
+    extra = {}
+    if not args.decode_only and not args.no_extra:
+        for name in ("esm2-650m-ragged-b64", "esm2-3b-36layer-b16-seq8192"):
+            extra[name] = workload_line(torch, tq, synth, name, args.replays, args.cpu_seconds / 3,
+                                        cpu=not args.no_cpu_baseline)
+            torch.cuda.empty_cache()
+
+    calibration = None
+    if not args.decode_only:
+        from paper_2603_26110_amd import quality
+        calibration = quality.calibration_timing()
+        calibration = {"heads": calibration["heads"], "calibration_vectors_per_head": calibration["ncal"],
+                       "seconds": round(calibration["seconds"], 3),
+                       "what": "head-wise SVD rotation and separate K and V tables of the 33 x 20 heads "
+                               "of ESM-2 650M on the GPU (Sec. 3.2 quotes 2-5 min for its calibration)"}
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(k_all, v_all, S, lut, pi, q, L, H, slots, n_ctx, args.cpu_seconds)
@@ -285,6 +336,12 @@ def main():
         "kv_pct_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "decode_steps_per_s": round(1e3 / ms_per_step, 1),
         "step_event_ms": round(step_ms, 5),
+        "step_ms_median": spread["median"],
+        "step_ms_p10": spread["p10"],
+        "step_ms_p90": spread["p90"],
+        "step_spread_replays": spread["replays"],
+        "per_layer_launches": per_layer,
+        "hbm_read_probe": probe,
         "two_call_step_ms": None if two_call_ms is None else round(two_call_ms, 5),
         "decode_attend_ms": round(attend_ms, 5),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -295,6 +352,8 @@ def main():
                                 "decode_kernel<8, false> (one launch per tq_decode_step call)"),
                      "alg_bytes_per_launch": int(alg_bytes)},
         "cpu_baseline": cpu,
+        "configs": extra or None,
+        "calibration": calibration,
         "prefill_quantize": prefill,
         "two_step_baseline": two_step,
         "fp16_attention_baseline": fp16_base,
@@ -303,6 +362,332 @@ def main():
                                               "NVIDIA GPU on Colab, model and precision unstated (Table 6)"},
     }
     print(json.dumps(line))
+
+
+def replay_spread(torch, graph, stream, K, replays):
+    """Per-step time of `replays` further replays of the K-step graph (HIP
+    events on the graph's stream around each replay): median, p10, p90."""
+    per = []
+    for _ in range(max(1, replays)):
+        a_, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            a_.record(stream)
+            graph.replay()
+            b_.record(stream)
+        torch.cuda.synchronize()
+        per.append(a_.elapsed_time(b_) / K)
+    per = np.asarray(per)
+    return {"median": round(float(np.median(per)), 5), "p10": round(float(np.percentile(per, 10)), 5),
+            "p90": round(float(np.percentile(per, 90)), 5), "replays": len(per)}
+
+
+def per_layer_launches(torch, tq, params, reps, L, n_ctx, pos_new, slot0, cached, lut_d, S_d, K, stream,
+                       kv_bytes):
+    """The same decode step as one tq_decode_step launch per layer (33 calls of
+    20 units each, as a model that decodes layer by layer would make them),
+    captured in one graph of K steps; each call's split-K workspace is
+    preallocated and left zero by the kernel."""
+    R = len(reps)
+    p1 = params
+    need = tq.decode_workspace_bytes(p1, 1, 1, n_ctx)
+    ws = torch.zeros(max(need, 16), dtype=torch.uint8, device="cuda")
+
+    def step(r):
+        d = reps[r]
+        for l in range(L):
+            tq.decode_step(p1, d["cache"], d["q"][l:l + 1], d["k1"][l:l + 1], d["v1"][l:l + 1], pos_new, slot0,
+                           cached, n_ctx, d["pi"], lut_d, lut_d, S_d, layer0=l, out=d["out"][l:l + 1], workspace=ws)
+
+    for r in range(2):
+        step(r % R)
+    torch.cuda.synchronize()
+    g_ = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_, stream=stream):
+        for k in range(K):
+            step(k % R)
+    g_.replay()
+    torch.cuda.synchronize()
+    sp = replay_spread(torch, g_, stream, K, 5)
+    del g_
+    return {"launches_per_step": L, "units_per_launch": params.num_heads, "step_ms_median": sp["median"],
+            "step_ms_p10": sp["p10"], "step_ms_p90": sp["p90"],
+            "kv_gbs": round(kv_bytes / (sp["median"] * 1e-3) / 1e9, 1)}
+
+
+def hbm_read_probe(torch, tq, nbytes, replica_bytes, K):
+    """A plain streaming read of as many bytes as one decode step's algorithmic
+    bytes, in the same run (the library's tq_read_probe: 16-byte loads, four
+    in flight per thread), over rotating replicas so that every call reads
+    HBM; the best of a few grid sizes. The ceiling a read of this size reaches
+    on this GPU, next to which the fused step's rate is judged."""
+    n = int(nbytes) // 16 * 16
+    R = max(2, math.ceil(replica_bytes / n))
+    bufs = [torch.ones(n // 4, dtype=torch.int32, device="cuda") for _ in range(R)]
+    sink = torch.zeros(65536, dtype=torch.int32, device="cuda")
+    out = {"bytes": n, "replicas": R, "calls": K}
+
+    def timed(fn):
+        for r in range(R):
+            fn(bufs[r])
+        torch.cuda.synchronize()
+        best = None
+        for rep in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for k in range(K):
+                fn(bufs[k % R])
+            e1.record()
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / K
+            best = ms if best is None else min(best, ms)
+        return n / (best * 1e-3) / 1e9
+
+    best = None
+    for blocks in (512, 1024, 2048, 4096):
+        gbs = timed(lambda x, b=blocks: tq.read_probe(x, b, sink))
+        out[f"blocks_{blocks}_gbs"] = round(gbs, 1)
+        if best is None or gbs > best[1]:
+            best = (blocks, gbs)
+    out["blocks"], out["gbs"] = best[0], round(best[1], 1)
+    out["frac_of_peak"] = round(best[1] / HBM_PEAK_GBS, 4)
+    del bufs
+    torch.cuda.empty_cache()
+    return out
+
+
+def workload_line(torch, tq, synth, name, replays, cpu_seconds, eager=False, cpu=True):
+    """Decode steps of a batched workload: the ragged batch of 64 ESM-2 650M
+    sequences, or the ESM-2 3B shape (16 sequences of 8192 tokens, head-wise
+    SVD rotations and calibrated tables). The cache is prefilled with
+    tq_quantize_pack from keys and values drawn on the GPU; then K steps
+    (each one tq_decode_step over every layer, sequence and head: append the
+    sequence's next token and attend) are captured in one graph and replayed.
+    The cache itself (1.7 GB and 13.7 GB) is far larger than the Infinity
+    Cache, so no replicas are needed. Figures: KV GB/s and the roofline
+    fraction of the step's algorithmic bytes, steps/s, and the oracle
+    decoding a seeded sample of units from the GPU's cache bytes (timed with
+    all threads and with one, and compared with the GPU's output)."""
+    from oracle import oracle
+    wl = synth.WORKLOADS[name]
+    dev = torch.device("cuda:0")
+    L, H, B = wl.layers, wl.heads, wl.batch
+    K = wl.decode_steps if wl.decode_steps > 1 else 20
+    g = synth.rng(wl.seed)
+    ch = synth.outlier_channels(g, L, H)
+    S = synth.qjl_matrix(g)
+    lens = (synth.ragged_lengths(g, B, *wl.ragged) if wl.ragged else np.full(B, wl.seq, np.int64)).astype(np.int32)
+    offs, slots = synth.tile_aligned_offsets(lens, extra=K)
+    caps = np.diff(np.append(offs, slots))
+    positions = int(lens.max()) + K + 64
+    cs = tq.rope_table(positions)
+    io = torch.float16
+    t_ = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    S_d = t_(S)
+
+    # rotations and tables
+    t0 = time.perf_counter()
+    if wl.rotation == "svd":
+        pi_d = torch.empty((L, H, 64, 64), dtype=torch.float32, device=dev)
+        lk_d = torch.empty((L, H, 8), dtype=torch.float32, device=dev)
+        lv_d = torch.empty((L, H, 8), dtype=torch.float32, device=dev)
+        for l in range(L):
+            gen = synth.device_generator(wl.seed + 7919, l, dev)
+            ck = synth.keys_on(gen, 1, wl.calib_vectors, H, ch[l], io, dev)[0].float()
+            cv = synth.values_on(gen, 1, wl.calib_vectors, H, io, dev)[0].float()
+            cpos = torch.randint(0, wl.seq, (wl.calib_vectors,), generator=gen, device=dev)
+            c_, s_ = cs[cpos, :, 0].unsqueeze(1), cs[cpos, :, 1].unsqueeze(1)
+            a_, b_ = ck[..., 0::2], ck[..., 1::2]
+            kr = torch.empty_like(ck)
+            kr[..., 0::2] = a_ * c_ - b_ * s_
+            kr[..., 1::2] = a_ * s_ + b_ * c_
+            xk = kr.transpose(0, 1).contiguous()
+            p_, _ = tq.calibrate_rotation(xk)
+            pi_d[l] = p_
+            lk_d[l] = tq.calibrate_lut(xk, p_)
+            lv_d[l] = tq.calibrate_lut(cv.transpose(0, 1).contiguous(), p_)
+    else:
+        pi_d = t_(synth.rotations(g, L, H))
+        lk_d = lv_d = t_(np.broadcast_to(synth.GAUSS_LEVELS_MAX1960, (L, H, 8)).copy())
+    torch.cuda.synchronize()
+    calib_s = time.perf_counter() - t0
+
+    # prefill, and the K steps' queries and new tokens
+    params = tq.Params(L, H, cs, io_dtype=io, flags=tq.V_ROTATE)
+    cache = tq.Cache(L, H, slots, device=dev)
+    q_all = torch.empty((K, L, B, H, 64), dtype=io, device=dev)
+    k_all = torch.empty_like(q_all)
+    v_all = torch.empty_like(q_all)
+    offs_d = t_(offs)
+    tmax = int(lens.max())
+    same = bool(np.all(lens == lens[0]))
+    bidx = torch.arange(B, device=dev)
+    lens_d = t_(lens.astype(np.int64))
+    pf_ms = 0.0
+    for l in range(L):
+        gen = synth.device_generator(wl.seed, l, dev)
+        kl = synth.keys_on(gen, B, tmax + K, H, ch[l], io, dev)
+        vl = synth.values_on(gen, B, tmax + K, H, io, dev)
+        for s in range(K):
+            q_all[s, l] = synth.queries_on(gen, B, H, io, dev)
+            k_all[s, l] = kl[bidx, lens_d + s]
+            v_all[s, l] = vl[bidx, lens_d + s]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if same:
+            kp, vp = kl[None, :, :tmax].contiguous(), vl[None, :, :tmax].contiguous()
+            e0.record()
+            tq.quantize_pack(params, cache, kp, vp, t_(np.zeros(B, np.int32)), offs_d, pi_d, lk_d, lv_d, S_d,
+                             layer0=l)
+            e1.record()
+        else:
+            parts = [(kl[b:b + 1, :int(lens[b])][None].contiguous(), vl[b:b + 1, :int(lens[b])][None].contiguous())
+                     for b in range(B)]
+            e0.record()
+            for b, (kp, vp) in enumerate(parts):
+                tq.quantize_pack(params, cache, kp, vp, t_(np.zeros(1, np.int32)), offs_d[b:b + 1], pi_d, lk_d,
+                                 lv_d, S_d, layer0=l)
+            e1.record()
+        torch.cuda.synchronize()
+        pf_ms += e0.elapsed_time(e1)
+        del kl, vl
+    torch.cuda.empty_cache()
+
+    pos = [t_((lens + s).astype(np.int32)) for s in range(K)]
+    outs = torch.empty((K, L, B, H, 64), dtype=io, device=dev)
+    ws_need = tq.decode_workspace_bytes(params, B, L, tmax + K)
+    ws = torch.zeros(max(ws_need, 16), dtype=torch.uint8, device=dev)
+
+    def step(s):
+        tq.decode_step(params, cache, q_all[s], k_all[s], v_all[s], pos[s], offs_d, pos[s], tmax + s + 1, pi_d,
+                       lk_d, lv_d, S_d, out=outs[s], workspace=ws)
+
+    for s in range(K):
+        step(s)
+    torch.cuda.synchronize()
+    if eager:
+        for s in range(K):
+            step(s)
+        torch.cuda.synchronize()
+        return {"workload": name, "eager_steps": K}
+    stream = torch.cuda.Stream(device=dev)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        for s in range(K):
+            step(s)
+    graph.replay()
+    torch.cuda.synchronize()
+    sp = replay_spread(torch, graph, stream, K, replays)
+    del graph
+
+    units = L * B * H
+    tok = float(np.sum(lens)) * L * H          # token-heads cached before the first step
+    kv_bytes = (tok + units * (K + 1) / 2.0) * 72       # average over the K steps
+    alg_bytes = kv_bytes + L * H * 64 * 64 * 4 + 64 * 64 * 4 + L * H * 8 * 4 * 2 + units * 64 * 2 * 4 + units * 72
+    ms = sp["median"]
+    line = {"workload": name, "layers": L, "heads": H, "batch": B,
+            "cached_tokens": ({"min": int(lens.min()), "mean": round(float(lens.mean()), 1), "max": int(lens.max())}
+                              if wl.ragged else int(lens[0])),
+            "steps": K, "rotation": wl.rotation, "replays": sp["replays"],
+            "step_ms_median": ms, "step_ms_p10": sp["p10"], "step_ms_p90": sp["p90"],
+            "kv_gbs": round(kv_bytes / (ms * 1e-3) / 1e9, 1),
+            "decode_steps_per_s": round(1e3 / ms, 1),
+            "roofline": {"bound": "hbm", "achieved": round(alg_bytes / (ms * 1e-3) / 1e9, 1), "peak": HBM_PEAK_GBS,
+                         "unit": "GB/s", "frac": round(alg_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                         "alg_bytes_per_launch": int(alg_bytes),
+                         "kernel": "decode_kernel<8, false> (one launch per tq_decode_step call)"},
+            "calibration_s": round(calib_s, 3),
+            "prefill_quantize_ms": round(pf_ms, 3),
+            "prefill_token_heads": int(tok)}
+    if cpu:
+        line["cpu_baseline"] = oracle_sample(torch, oracle, cache, pi_d, lk_d, lv_d, S, q_all[K - 1], outs[K - 1],
+                                             lens + K, offs, caps, L, H, B, positions, cpu_seconds, wl.seed)
+    del cache, q_all, k_all, v_all, outs
+    torch.cuda.empty_cache()
+    return line
+
+
+def oracle_sample(torch, oracle, cache, pi_d, lk_d, lv_d, S, q_last, out_last, n_att, offs, caps, L, H, B,
+                  positions, seconds, seed):
+    """The oracle's fp64 decode of a seeded sample of units, from the GPU
+    cache's bytes after the timed steps (each sequence's units in a cache of
+    their own): timed with all of the oracle's threads and with one, in KV
+    GB/s, and compared with the GPU's output of the last step."""
+    g = np.random.default_rng(seed + 17)
+    seqs = sorted(set(int(x) for x in g.choice(B, size=min(2, B), replace=False)))
+    per_seq = 16
+    jobs = []
+    cs = oracle.rope_table(positions)
+    kc, vc, sc = cache.k_codes, cache.v_codes, cache.scalars
+    slots = cache.slots
+    for b in seqs:
+        picks = sorted(set((int(g.integers(L)), int(g.integers(H))) for _ in range(per_seq)))
+        cap = int(caps[b])
+        oc = oracle.Cache(1, len(picks), cap)
+        for i, (l, h) in enumerate(picks):
+            base = (l * H + h) * slots + int(offs[b])
+            oc.k[i * cap * 32:(i + 1) * cap * 32] = kc[base * 32:(base + cap) * 32].cpu().numpy()
+            oc.v[i * cap * 32:(i + 1) * cap * 32] = vc[base * 32:(base + cap) * 32].cpu().numpy()
+            oc.s[i * cap * 4:(i + 1) * cap * 4] = sc[base * 4:(base + cap) * 4].cpu().numpy().view(np.uint16)
+        ls = [l for l, _ in picks]
+        hs = [h for _, h in picks]
+        q = q_last[ls, b, hs].float().cpu().numpy()[None, None]
+        pi = pi_d[ls, hs].cpu().numpy()[None]
+        lk = lk_d[ls, hs].cpu().numpy()[None]
+        lv = lv_d[ls, hs].cpu().numpy()[None]
+        ref_gpu = out_last[ls, b, hs].float().cpu().numpy()
+        n = int(n_att[b])
+        jobs.append((oc, q, pi, lk, lv, ref_gpu, n, len(picks)))
+
+    def run_all():
+        errs = []
+        for oc, q, pi, lk, lv, ref_gpu, n, _ in jobs:
+            o = oracle.decode(oc, oracle.V_ROTATE, cs, q, [n - 1], [0], [n], pi, lk, lv, S)
+            errs.append(float(np.max(np.abs(o[0, 0] - ref_gpu))))
+        return max(errs)
+
+    kv = sum(cnt * n * 72 for _, _, _, _, _, _, n, cnt in jobs)
+    res = {"kind": "oracle", "unit": "GB/s", "nproc": len(os.sched_getaffinity(0)),
+           "sample": f"{sum(j[7] for j in jobs)} (layer, head) units of sequences {seqs} (seeded), "
+                     f"fp64 decode of the GPU cache's bytes after the timed steps"}
+    threads = oracle.max_threads()
+    for label, nt in (("all", threads), ("one", 1)):
+        oracle.set_threads(nt)
+        runs, tt, err = 0, 0.0, 0.0
+        while tt < seconds / 2 or runs == 0:
+            t0 = time.perf_counter()
+            err = run_all()
+            tt += time.perf_counter() - t0
+            runs += 1
+        gbs = kv * runs / tt / 1e9
+        if label == "all":
+            res["value"], res["cores"] = round(gbs, 4), nt
+        else:
+            res["value_1thread"] = round(gbs, 4)
+        res["max_abs_err_vs_gpu"] = round(err, 6)
+    oracle.set_threads(threads)
+    return res
+
+
+def only_kernel(torch, tq, which, K, params, reps, base_cache, t_, k_all, v_all, T, n_ctx, L, H, slots, pi_d,
+                lut_d, S_d, zero_i32, zero_i64):
+    """K eager launches of one kernel on the headline shape, for counter
+    collection: the prefill quantizer (tq_quantize_pack of the T cached
+    tokens of every unit) or the dequantize baseline (tq_dequantize of the
+    n_ctx tokens of every unit)."""
+    if which == "prefill":
+        pf_cache = tq.Cache(L, H, slots, device="cuda")
+        k_pf, v_pf = t_(k_all[:, :, :T]), t_(v_all[:, :, :T])
+        for _ in range(K):
+            tq.quantize_pack(params, pf_cache, k_pf, v_pf, zero_i32, zero_i64, pi_d, lut_d, lut_d, S_d)
+    else:
+        shape = (L, 1, H, n_ctx, 64)
+        ko = torch.empty(shape, dtype=torch.float16, device="cuda")
+        vo = torch.empty(shape, dtype=torch.float16, device="cuda")
+        sl = torch.tensor([n_ctx], dtype=torch.int32, device="cuda")
+        for k in range(K):
+            tq.dequantize(params, reps[k % len(reps)]["cache"], zero_i64, sl, n_ctx, lut_d, lut_d, S_d,
+                          k_out=ko, v_out=vo)
+    torch.cuda.synchronize()
+    print(json.dumps({"only": which, "launches": K}))
 
 
 def fp16_attention_baseline(torch, units, n_ctx, replica_bytes, K):
@@ -441,7 +826,7 @@ def cpu_baseline(k_all, v_all, S, lut, pi, q, L, H, slots, n_ctx, seconds):
     oracle.quantize_pack(oc, 1, cs, k_all[:, :, :T], v_all[:, :, :T], [0], [0], pi, lut, lut, S)
     k_new, v_new = k_all[:, :, T:T + 1], v_all[:, :, T:T + 1]
     qf = np.asarray(q, np.float32)
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = oracle.max_threads()
 
     def run(units):
         oracle.quantize_pack(oc, 1, cs, k_new, v_new, [T], [T], pi, lut, lut, S)
@@ -465,9 +850,24 @@ def cpu_baseline(k_all, v_all, S, lut, pi, q, L, H, slots, n_ctx, seconds):
         t_total += time.perf_counter() - t0
         runs += 1
     kv = units_per_run * n_ctx * 72 * runs
+    # the same step with one thread, over a leading subset of units (the
+    # append is serial anyway)
+    oracle.set_threads(1)
+    one_units = np.arange(max(1, min(L * H, units_per_run // max(1, threads))))
+    t1, runs1 = 0.0, 0
+    while t1 < seconds / 3 or runs1 == 0:
+        t0 = time.perf_counter()
+        run(one_units)
+        t1 += time.perf_counter() - t0
+        runs1 += 1
+    oracle.set_threads(threads)
     return {"value": round(kv / t_total / 1e9, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "nproc": len(os.sched_getaffinity(0)), "os_cpu_count": os.cpu_count(),
+            "value_1thread": round(len(one_units) * n_ctx * 72 * runs1 / t1 / 1e9, 4),
             "sample": f"{runs} oracle step(s): append of the new token to all {L * H} (layer, head) units, "
-                      f"then fp64 decode of {units_per_run} of them over {n_ctx} tokens, {t_total:.1f} s"}
+                      f"then fp64 decode of {units_per_run} of them over {n_ctx} tokens, {t_total:.1f} s "
+                      f"({threads} threads); one thread: {runs1} step(s) decoding {len(one_units)} units, "
+                      f"{t1:.1f} s"}
 
 
 if __name__ == "__main__":

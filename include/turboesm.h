@@ -372,6 +372,16 @@ TQ_API tq_status tq_calibrate_ebar(const float* x, int32_t nheads, int32_t ncal,
  * made after the call. Returns the previous limit. */
 TQ_API int32_t tq_set_step_wait_limit(int32_t limit);
 
+/* Measurement helper, not part of the method: a plain streaming read of
+ * `bytes` bytes at `data` (device, 16-byte aligned, bytes a multiple of 16)
+ * by `blocks` blocks of 256 threads (1..65536), each thread keeping four
+ * 16-byte loads in flight. Nothing is written except, in the never-taken case
+ * that a block's folded data equals a fixed constant, one word of `sink`
+ * (device, >= blocks words). Timing it over a buffer as large as a decode
+ * step's bytes gives the read rate the GPU reaches for a transfer of that
+ * size, next to which a decode kernel's rate is judged. */
+TQ_API tq_status tq_read_probe(const void* data, int64_t bytes, int32_t blocks, uint32_t* sink, void* stream);
+
 /* Message of the last failing call on this thread ("" if none). */
 TQ_API const char* tq_last_error(void);
 

@@ -79,8 +79,19 @@ def lib():
                                  P, P, P, P, P, P, P, P, P, P, P, P, i64, i32, P]
         L.orc_dequantize.argtypes = [i32, i32, i64, u32, i32, i32, i32, P, P, i32,
                                      P, P, P, P, P, P, P, P, P]
+        L.orc_set_threads.argtypes = [i32]
+        L.orc_max_threads.restype = i32
         _lib = L
     return _lib
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's loops over units (timing only)."""
+    lib().orc_set_threads(int(n))
+
+
+def max_threads() -> int:
+    return int(lib().orc_max_threads())
 
 
 def _p(a: np.ndarray):

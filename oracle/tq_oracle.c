@@ -27,6 +27,7 @@
  * (closed forms, library routines, brute force, worked examples).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -502,6 +503,11 @@ static void decode_unit_twostep(const unit_ctx* u, uint32_t flags, double scale,
  * is the flat index (li*B + b)*H + h), or over all units when units == NULL.
  * q: [nl][B][H][64] floats; out: [nl][B][H][64] doubles (only listed units are
  * written). twostep selects the two-step form. */
+/* Threads of the OpenMP loops over units, for timing the oracle (its results
+ * do not depend on the count). */
+void orc_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
+int orc_max_threads(void) { return omp_get_max_threads(); }
+
 void orc_decode(int L, int H, int64_t slots, uint32_t flags, double scale,
                 const float* cs, int rope_positions, const float* q, int B,
                 int layer0, int nl, const int32_t* qpos, const int64_t* sslot0,

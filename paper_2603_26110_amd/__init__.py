@@ -21,6 +21,7 @@ import torch
 __all__ = [
     "Params", "Cache", "TQError", "rope_table", "quantize_pack", "decode_attend", "decode_step", "dequantize",
     "decode_attend_noalloc", "decode_workspace_bytes", "calibrate_rotation", "calibrate_lut", "calibrate_ebar", "set_step_wait_limit",
+    "read_probe",
     "cache_bytes", "last_error", "version",
     "V_ROTATE", "V_QJL", "QJL_PAPER", "ROPE_HALF", "INPUT_ROTATED", "OUT_FP32", "lib_path",
 ]
@@ -86,6 +87,8 @@ def _load():
     L.tq_decode_attend_noalloc.restype = i32
     L.tq_set_step_wait_limit.argtypes = [i32]
     L.tq_set_step_wait_limit.restype = i32
+    L.tq_read_probe.argtypes = [P, i64, i32, P, P]
+    L.tq_read_probe.restype = i32
     _lib = L
     return L
 
@@ -384,6 +387,19 @@ def calibrate_ebar(x: torch.Tensor, lut: torch.Tensor, pi=None, out=None, stride
     _check(L.tq_calibrate_ebar(_ptr(x), nh, ncal, _ptr(pi), _ptr(lut), _ptr(out), int(stride),
                                _stream(x.device)))
     return out
+
+
+def read_probe(data: torch.Tensor, blocks: int, sink: torch.Tensor) -> None:
+    """Streaming read of every byte of `data` (a measurement, not part of the
+    method; see tq_read_probe). sink: int32 device tensor of >= blocks words."""
+    L = _load()
+    if not data.is_cuda or not data.is_contiguous():
+        raise ValueError("data must be a contiguous device tensor")
+    _dev(sink, "sink", torch.int32)
+    if sink.numel() < blocks:
+        raise ValueError("sink must hold >= blocks words")
+    _check(L.tq_read_probe(_ptr(data), data.numel() * data.element_size(), int(blocks), _ptr(sink),
+                           _stream(data.device)))
 
 
 def set_step_wait_limit(limit: int) -> int:

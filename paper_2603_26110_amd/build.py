@@ -18,7 +18,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 OBJ_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libturboesm.so")
-SOURCES = ["tq_api.hip", "tq_quantize.hip", "tq_decode.hip", "tq_dequant.hip", "tq_calibrate.hip"]
+SOURCES = ["tq_api.hip", "tq_quantize.hip", "tq_decode.hip", "tq_dequant.hip", "tq_calibrate.hip",
+           "tq_probe.hip"]
 ARCH = os.environ.get("TQ_OFFLOAD_ARCH", "gfx950")
 
 CFLAGS = [

@@ -98,6 +98,15 @@ int32_t tq_set_step_wait_limit(int32_t limit) {
 
 const char* tq_version(void) { return "turboesm-gfx950 0.1.0"; }
 
+tq_status tq_read_probe(const void* data, int64_t bytes, int32_t blocks, uint32_t* sink, void* stream) {
+  if (bytes == 0) return ok();
+  if (!data || !sink) return fail(TQ_ERR_ARG, "tq_read_probe: data and sink must not be NULL");
+  if (bytes < 0 || bytes % 16 != 0) return fail(TQ_ERR_ARG, "tq_read_probe: bytes must be a multiple of 16");
+  if (!aligned(data, 16) || !aligned(sink, 4)) return fail(TQ_ERR_ALIGN, "tq_read_probe: data must be 16-byte aligned");
+  if (blocks < 1 || blocks > 65536) return fail(TQ_ERR_ARG, "tq_read_probe: blocks must be in [1, 65536]");
+  return hip_status(tq::launch_read_probe(data, bytes, blocks, sink, (hipStream_t)stream), "tq_read_probe launch");
+}
+
 int64_t tq_cache_bytes(int32_t num_layers, int32_t num_heads, int64_t slots) {
   if (num_layers < 0 || num_heads < 0 || slots < 0) return -1;
   return (int64_t)num_layers * num_heads * slots * 72;

@@ -105,4 +105,8 @@ hipError_t launch_calibrate_ebar(const float* x, int nheads, int ncal, const flo
 hipError_t launch_calibrate(const float* x, int nheads, int ncal, float* pi_out,
                             float* sing_out, hipStream_t st);
 
+// Streaming read of `bytes` (a multiple of 16) at `data` by `blocks` blocks
+// (tq_probe.hip; a measurement, not part of the method).
+hipError_t launch_read_probe(const void* data, int64_t bytes, int blocks, uint32_t* sink, hipStream_t st);
+
 }  // namespace tq

@@ -39,8 +39,8 @@ def test_header_declares_the_entry_points():
     assert _declared_functions() == sorted([
         "tq_cache_bytes", "tq_rope_table", "tq_quantize_pack", "tq_decode_attend", "tq_decode_step",
         "tq_dequantize", "tq_decode_workspace_bytes", "tq_calibrate_rotation", "tq_calibrate_lut",
-        "tq_calibrate_ebar", "tq_set_step_wait_limit", "tq_decode_attend_noalloc", "tq_last_error",
-        "tq_version"])
+        "tq_calibrate_ebar", "tq_set_step_wait_limit", "tq_decode_attend_noalloc", "tq_read_probe",
+        "tq_last_error", "tq_version"])
 
 
 def test_library_exports_exactly_the_declared_symbols():
