@@ -132,13 +132,42 @@ __device__ __forceinline__ float nearest_level(float u, const Levels& L, float c
   return lv;
 }
 
+// The index alone, #{m : u > t_m} (the same count as nearest_level's), for a
+// caller that reads the level itself from a table in LDS: each comparison
+// goes into the count at once, so no lane mask stays live across the
+// elements of a vector (64 unrolled select chains keep so many masks live
+// that they spill).
+__device__ __forceinline__ uint32_t level_index(float u, const Levels& L) {
+  // t_m < u sets VCC (false for a NaN u, like u > t_m), which the next
+  // instruction adds into the count
+  uint32_t i;
+  asm("v_cmp_lt_f32 vcc, %1, %8\n\t"
+      "v_cndmask_b32 %0, 0, 1, vcc\n\t"
+      "v_cmp_lt_f32 vcc, %2, %8\n\t"
+      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
+      "v_cmp_lt_f32 vcc, %3, %8\n\t"
+      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
+      "v_cmp_lt_f32 vcc, %4, %8\n\t"
+      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
+      "v_cmp_lt_f32 vcc, %5, %8\n\t"
+      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
+      "v_cmp_lt_f32 vcc, %6, %8\n\t"
+      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
+      "v_cmp_lt_f32 vcc, %7, %8\n\t"
+      "v_addc_co_u32 %0, vcc, 0, %0, vcc"
+      : "=&v"(i)
+      : "s"(L.t0), "s"(L.t1), "s"(L.t2), "s"(L.t3), "s"(L.t4), "s"(L.t5), "s"(L.t6), "v"(u)
+      : "vcc");
+  return i;
+}
+
 struct QuantOut {
   uint32_t n16, g16;
   float g;                 // ||r|| in binary32 (before the fp16 store)
 };
 
 template <bool KEY_WORDS>
-__device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Levels& L,
+__device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Levels& L, const float* lev,
                                                   const float* S, int sign_mode,
                                                   uint32_t (&words)[8]) {
   float s = 0.0f;
@@ -148,12 +177,11 @@ __device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Level
   const float inv = (n == 0.0f) ? 0.0f : 8.0f / n;
 #pragma unroll
   for (int w = 0; w < 8; ++w) words[w] = 0u;
-  TQ_PIN_LEVELS(L);
 #pragma unroll
   for (int i = 0; i < kDim; ++i) {
     const float u = xh[i] * inv;
-    uint32_t idx;
-    const float lv = nearest_level(u, TQ_LEVELS(L), &idx);
+    const uint32_t idx = level_index(u, L);
+    const float lv = lev[idx];   // the level c[idx], from the table in LDS
     words[i >> 3] |= idx << ((KEY_WORDS ? 3 : 4) * (i & 7));
     xh[i] = u - lv;   // residual r_i
   }

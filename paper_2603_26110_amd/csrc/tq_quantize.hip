@@ -243,45 +243,65 @@ __device__ __forceinline__ void rotate_tokens(float (&out)[kDim], const QuantArg
 __device__ __forceinline__ uint64_t projected_signs(float (&x)[kDim], float g, const _Float16* sh,
                                                     const _Float16* sl, const float* s_Sn, const float* S,
                                                     int lane) {
-  const int hh = lane >> 5;
+  const int n = lane & 31, hh = lane >> 5;
   float m = 0.0f;
 #pragma unroll
   for (int k = 0; k < kDim; ++k) m = fmaxf(m, fabsf(x[k]));
   const float sc = unit_scale(m);                    // token l's scale
   const float sc_other = __shfl_xor(sc, 32, 64);     // token l ^ 32's
   const float sc0 = hh ? sc_other : sc, sc1 = hh ? sc : sc_other;   // tokens n, 32 + n
-  SplitOps ops;
+  // Step q's operands are built just before its products, from swapped
+  // copies (x keeps the lane-per-token layout for the chain below).
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) { acc[0][0][r] = 0.0f; acc[1][0][r] = 0.0f; acc[0][1][r] = 0.0f; acc[1][1][r] = 0.0f; }
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
+    float b0[8], b1[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[16 * q + j]),
                                                        __float_as_uint(x[16 * q + 8 + j]), false, false);
-      x[16 * q + j] = __uint_as_float(sw[0]);       // token n, dimension 16q + 8h + j
-      x[16 * q + 8 + j] = __uint_as_float(sw[1]);   // token 32 + n, dimension 16q + 8h + j
+      b0[j] = __uint_as_float(sw[0]);   // token n, dimension 16q + 8h + j
+      b1[j] = __uint_as_float(sw[1]);   // token 32 + n, dimension 16q + 8h + j
     }
-    split8(&x[16 * q], sc0, ops.hi[0][q], ops.lo[0][q]);
-    split8(&x[16 * q + 8], sc1, ops.hi[1][q], ops.lo[1][q]);
+    half8 h0, l0, h1, l1;
+    split8(b0, sc0, h0, l0);
+    split8(b1, sc1, h1, l1);
+    int o = n * kHPitch + 16 * q + 8 * hh;
+    asm volatile("" : "+v"(o));
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[16 * q + j]),
-                                                       __float_as_uint(x[16 * q + 8 + j]), false, false);
-      x[16 * q + j] = __uint_as_float(sw[0]);
-      x[16 * q + 8 + j] = __uint_as_float(sw[1]);
+    for (int mb = 0; mb < 2; ++mb) {
+      const half8 ah = *reinterpret_cast<const half8*>(sh + o + 32 * mb * kHPitch);
+      const half8 al = *reinterpret_cast<const half8*>(sl + o + 32 * mb * kHPitch);
+      acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, h0, acc[mb][0], 0, 0, 0);
+      acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, l0, acc[mb][0], 0, 0, 0);
+      acc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_f16(al, h0, acc[mb][0], 0, 0, 0);
+      acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, h1, acc[mb][1], 0, 0, 0);
+      acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah, l1, acc[mb][1], 0, 0, 0);
+      acc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_f16(al, h1, acc[mb][1], 0, 0, 0);
     }
   }
-  f32x16 acc[2][2];
-  split_products(ops, sh, sl, lane, acc);
-  float p[kDim];
-  to_lane_per_token(acc, p);
+  // the result reaches lane l (token l) one register pair at a time and is
+  // tested at once (no 64-value copy of it is held)
   uint64_t bits = 0, flagged = 0;
   const float gb = g * sc * 0x1p-14f;
 #pragma unroll
-  for (int i = 0; i < kDim; ++i) {
-    const bool sure = fabsf(p[i]) > s_Sn[i] * gb;
-    bits |= (uint64_t)((sure && !(p[i] < 0.0f)) ? 1u : 0u) << i;
-    flagged |= (uint64_t)(sure ? 0u : 1u) << i;
-  }
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[mb][0][r]),
+                                                       __float_as_uint(acc[mb][1][r]), false, false);
+      const int d = 32 * mb + 8 * (r >> 2) + (r & 3);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int i = d + 4 * e;
+        const float pv = __uint_as_float(sw[e]);
+        const bool sure = fabsf(pv) > s_Sn[i] * gb;
+        bits |= (uint64_t)((sure && !(pv < 0.0f)) ? 1u : 0u) << i;
+        flagged |= (uint64_t)(sure ? 0u : 1u) << i;
+      }
+    }
   // rows inside the band, any lane: the fixed-order chain (wave-uniform row)
   uint64_t any = flagged;
 #pragma unroll
@@ -325,6 +345,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   __shared__ float s_Sn[kDim];                                               // ||sigma_i S_i||
   __shared__ float s_sig[kDim];                                              // sigma_i
   __shared__ uint32_t s_vt[4][kDim * 8];
+  __shared__ float s_lev[2][8];                                              // K and V levels
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
   const int h = blockIdx.y % a.H, b = blockIdx.y / a.H, li = blockIdx.z;
@@ -347,6 +368,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
     }
     s_sig[threadIdx.x] = sig;
     s_Sn[threadIdx.x] = sqrtf(ss);
+  } else if (threadIdx.x < kDim + 16) {
+    const int e = threadIdx.x - kDim;
+    s_lev[e >> 3][e & 7] = ((e >> 3) ? a.lut_v : a.lut_k)[lh * 8 + (e & 7)];
   }
   __syncthreads();
   for (int e = threadIdx.x; e < kDim * kDim / 4; e += blockDim.x) {
@@ -394,7 +418,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
     rotate_tokens<F16>(x, a, a.k, s_pih, s_pil, li, b, h, j0, lane, true);
   }
   uint32_t kw[8];
-  const QuantOut qk = quantize_lane<true>(x, Lk, nullptr, paper ? 2 : 3, kw);
+  const QuantOut qk = quantize_lane<true>(x, Lk, s_lev[0], nullptr, paper ? 2 : 3, kw);
   if (!paper) {
     const uint64_t sb = projected_signs(x, qk.g, s_sh, s_sl, s_Sn, a.qjl_s, lane);
 #pragma unroll
@@ -417,7 +441,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
     for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.v, row + i, F16) : 0.0f;
   }
   uint32_t vw[8];
-  const QuantOut qv = quantize_lane<false>(x, Lv, nullptr, (VQJL && !paper) ? 3 : vsign, vw);
+  const QuantOut qv = quantize_lane<false>(x, Lv, s_lev[1], nullptr, (VQJL && !paper) ? 3 : vsign, vw);
   if (VQJL && !paper) {
     const uint64_t sb = projected_signs(x, qv.g, s_sh, s_sl, s_Sn, a.qjl_s, lane);
 #pragma unroll
