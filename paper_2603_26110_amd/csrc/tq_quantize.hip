@@ -343,7 +343,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   __shared__ __attribute__((aligned(16))) _Float16 s_sh[kDim * kHPitch];    // sigma_i S_i, fp16 parts
   __shared__ __attribute__((aligned(16))) _Float16 s_sl[kDim * kHPitch];
   __shared__ float s_Sn[kDim];                                               // ||sigma_i S_i||
-  __shared__ float s_sig[kDim];                                              // sigma_i
   __shared__ uint32_t s_vt[4][kDim * 8];
   __shared__ float s_lev[2][8];                                              // K and V levels
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -355,39 +354,47 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   const bool paper = (a.flags & kQjlPaper) != 0;
   const int vsign = VQJL ? (paper ? 2 : 1) : 0;   // (a V sign pass is compiled only where asked for)
 
-  if (threadIdx.x < kDim) {
-    // row i of S: its power-of-two scale and the norm of the scaled row
-    const float* srow = a.qjl_s + threadIdx.x * kDim;
-    float mx = 0.0f;
-    for (int k = 0; k < kDim; ++k) mx = fmaxf(mx, fabsf(srow[k]));
-    const float sig = unit_scale(mx);
-    float ss = 0.0f;
-    for (int k = 0; k < kDim; ++k) {
-      const float v = srow[k] * sig;
-      ss = fmaf(v, v, ss);
-    }
-    s_sig[threadIdx.x] = sig;
-    s_Sn[threadIdx.x] = sqrtf(ss);
-  } else if (threadIdx.x < kDim + 16) {
-    const int e = threadIdx.x - kDim;
-    s_lev[e >> 3][e & 7] = ((e >> 3) ? a.lut_v : a.lut_k)[lh * 8 + (e & 7)];
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < kDim * kDim / 4; e += blockDim.x) {
-    const int r = e >> 4, c4 = (e & 15) * 4;
-    const float4 pv = reinterpret_cast<const float4*>(a.pi + lh * kDim * kDim)[e];
-    const float4 sv = reinterpret_cast<const float4*>(a.qjl_s)[e];
-    const float sig = s_sig[r];
-    const float pa[4] = {pv.x, pv.y, pv.z, pv.w};
-    const float sa[4] = {sv.x * sig, sv.y * sig, sv.z * sig, sv.w * sig};
+  // Pi and S staged as fp16 parts, with the rows of S scaled by powers of
+  // two sigma_i and their norms: thread t takes row t / 4, columns
+  // 16 (t % 4) .. 16 (t % 4) + 15 of both (all eight 16-byte loads issued
+  // together); a row's four threads combine their maxima and sums by shuffles.
+  {
+    const int r = threadIdx.x >> 2, c0 = 16 * (threadIdx.x & 3);
+    const float4* pi4 = reinterpret_cast<const float4*>(a.pi + lh * kDim * kDim) + r * 16 + c0 / 4;
+    const float4* s4 = reinterpret_cast<const float4*>(a.qjl_s) + r * 16 + c0 / 4;
+    float pv[16], sv[16];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const _Float16 ph = (_Float16)pa[u], sh = (_Float16)sa[u];
-      s_pih[r * kHPitch + c4 + u] = ph;
-      s_pil[r * kHPitch + c4 + u] = (_Float16)(pa[u] - (float)ph);
-      s_sh[r * kHPitch + c4 + u] = sh;
-      s_sl[r * kHPitch + c4 + u] = (_Float16)(sa[u] - (float)sh);
+      const float4 p4 = pi4[u], q4 = s4[u];
+      pv[4 * u] = p4.x; pv[4 * u + 1] = p4.y; pv[4 * u + 2] = p4.z; pv[4 * u + 3] = p4.w;
+      sv[4 * u] = q4.x; sv[4 * u + 1] = q4.y; sv[4 * u + 2] = q4.z; sv[4 * u + 3] = q4.w;
     }
+    float mx = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) mx = fmaxf(mx, fabsf(sv[k]));
+    mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+    const float sig = unit_scale(mx);        // row r's scale (the same in its four threads)
+    float ss = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float v = sv[k] * sig;
+      ss = fmaf(v, v, ss);
+    }
+    ss += __shfl_xor(ss, 1, 64);
+    ss += __shfl_xor(ss, 2, 64);
+    if ((threadIdx.x & 3) == 0) s_Sn[r] = sqrtf(ss);   // bounds the guard band only
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const float sa = sv[k] * sig;
+      const _Float16 ph = (_Float16)pv[k], sh = (_Float16)sa;
+      s_pih[r * kHPitch + c0 + k] = ph;
+      s_pil[r * kHPitch + c0 + k] = (_Float16)(pv[k] - (float)ph);
+      s_sh[r * kHPitch + c0 + k] = sh;
+      s_sl[r * kHPitch + c0 + k] = (_Float16)(sa - (float)sh);
+    }
+    if (threadIdx.x < 16) s_lev[threadIdx.x >> 3][threadIdx.x & 7] =
+        ((threadIdx.x >> 3) ? a.lut_v : a.lut_k)[lh * 8 + (threadIdx.x & 7)];
   }
   const Levels Lk = load_levels(a.lut_k + lh * 8);
   const Levels Lv = load_levels(a.lut_v + lh * 8);
