@@ -468,7 +468,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   const uint64_t okmask = __ballot(ok);
-  if (okmask != 0) {
+  if (okmask == ~0ull && ((sbase + j0) & 7) == 0) {
+    // all 64 tokens, starting at a word boundary: eight whole words per
+    // dimension, nibble jj of word k from token 8k + jj
+    const int i = lane;
+    const int wsel = i >> 3, sh = 4 * (i & 7);
+    const int64_t g_first = (sbase + j0) >> 3;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      uint32_t word = 0;
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) word |= ((s_w[(8 * k + jj) * 8 + wsel] >> sh) & 15u) << (4 * jj);
+      const int64_t G = g_first + k;
+      const int64_t tile = G >> 3;
+      const int c = (int)((G & 7) >> 2);
+      *reinterpret_cast<uint32_t*>(vreg + tile_half_offset(tile, c, i) + (G & 3) * 4) = word;
+    }
+  } else if (okmask != 0) {
     const int i = lane;   // dimension handled by this lane
     const int64_t sA = sbase + j0;           // slot of token j0
     const int64_t g_first = sA >> 3, g_last = (sA + 63) >> 3;
