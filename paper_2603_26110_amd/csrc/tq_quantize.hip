@@ -334,8 +334,12 @@ __device__ __forceinline__ uint64_t projected_signs(float (&x)[kDim], float g, c
 // x = ceil(T/256), y = B*H, z = nlayers. LDS: Pi (pitch 68) for the
 // rotations, S (row-major, read by the quantizer as broadcasts) and one
 // 64 x 8 word buffer per wave for the V transpose.
-// Three waves per SIMD (168 registers; a few values spill) run faster than
-// two without spills: 225 against 392 us on the 650M-shape prefill.
+// Three waves per SIMD (168 registers, no spills for the default flags: the
+// key words and the value words wait in LDS while their signs are computed,
+// per-lane slot facts are recomputed where used, a level's index is counted
+// by compare-and-carry). Asking the compiler for four waves per SIMD gives
+// 232 registers (two waves) instead: the two rotations' and the projection's
+// 64-value results and their operands do not fit in 128.
 template <bool F16, bool VQJL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void quantize_tiles_kernel(QuantArgs a) {
   __shared__ __attribute__((aligned(16))) _Float16 s_pih[kDim * kHPitch];   // Pi, fp16 parts
@@ -404,14 +408,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   if (j0 >= a.T) return;                  // wave-uniform; no barrier follows
   // a (layer, head) whose K or V table is not strictly ascending is not written
   if (!levels_ascending(Lk) || !levels_ascending(Lv)) return;
-  const int j = j0 + lane;
   const int64_t sbase = a.slot0[b];
   const int pbase = a.pos0[b];
-  const int64_t slot = sbase + j;
-  const int pos = pbase + j;
-  const bool ok = j < a.T && slot >= 0 && slot < a.slots &&
-                  (rotated || (pos >= 0 && pos < a.rope_positions));
-  const int64_t row = ((((int64_t)li * a.B + b) * a.T + j) * a.H + h) * kDim;
+  // The lane's token facts (written or not, its slot, its input row) are
+  // recomputed where used, from an index the compiler cannot carry over,
+  // so that no 64-bit per-lane value stays live through the products.
+  auto lane_of = [&]() {
+    int ln;
+    asm volatile("v_mov_b32 %0, %1" : "=v"(ln) : "v"((int)threadIdx.x));
+    return ln & 63;
+  };
+  auto ok_of = [&](int jl) {
+    const int64_t sl = sbase + jl;
+    const int ps = pbase + jl;
+    return jl < a.T && sl >= 0 && sl < a.slots && (rotated || (ps >= 0 && ps < a.rope_positions));
+  };
+  auto row_of = [&](int jl) { return ((((int64_t)li * a.B + b) * a.T + jl) * a.H + h) * kDim; };
 
   uint8_t* kreg = a.k_codes + lh * a.slots * 32;
   uint8_t* vreg = a.v_codes + lh * a.slots * 32;
@@ -419,23 +431,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   // ---- K: RoPE and rotation, or a pre-rotated input as is
   float x[kDim];
   if (rotated) {
+    const int jl = j0 + lane;
+    const bool okl = ok_of(jl);
+    const int64_t row = row_of(jl);
 #pragma unroll
-    for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.k, row + i, false) : 0.0f;
+    for (int i = 0; i < kDim; ++i) x[i] = okl ? load_in(a.k, row + i, false) : 0.0f;
   } else {
     rotate_tokens<F16>(x, a, a.k, s_pih, s_pil, li, b, h, j0, lane, true);
   }
   uint32_t kw[8];
   const QuantOut qk = quantize_lane<true>(x, Lk, s_lev[0], nullptr, paper ? 2 : 3, kw);
   if (!paper) {
-    const uint64_t sb = projected_signs(x, qk.g, s_sh, s_sl, s_Sn, a.qjl_s, lane);
+    // the key words wait in this wave's transpose buffer while the signs are
+    // computed (registers)
+    uint32_t* s_k = s_vt[wave];
 #pragma unroll
-    for (int w = 0; w < 8; ++w) kw[w] |= (uint32_t)((sb >> (8 * w)) & 0xFFu) << 24;
+    for (int w = 0; w < 8; ++w) s_k[lane * 8 + w] = kw[w];
+    const uint64_t sb = projected_signs(x, qk.g, s_sh, s_sl, s_Sn, a.qjl_s, lane);
+    const int lk = lane_of();
+#pragma unroll
+    for (int w = 0; w < 8; ++w) kw[w] = s_k[lk * 8 + w] | (uint32_t)((sb >> (8 * w)) & 0xFFu) << 24;
   }
-  if (ok) {
+  const int jk = j0 + lane_of();
+  const int64_t slot = sbase + jk;
+  if (ok_of(jk)) {
     const int64_t tile = slot >> 6;
     const int r = (int)(slot & 63);
     *reinterpret_cast<uint4*>(kreg + tile_half_offset(tile, 0, r)) = make_uint4(kw[0], kw[1], kw[2], kw[3]);
     *reinterpret_cast<uint4*>(kreg + tile_half_offset(tile, 1, r)) = make_uint4(kw[4], kw[5], kw[6], kw[7]);
+    // [n_k, g_k] now (the V half of the slot's scalars follows), so that
+    // nothing of the key stays live through the value's products
+    reinterpret_cast<uint32_t*>(a.scalars + (lh * a.slots + slot) * 4)[0] = qk.n16 | (qk.g16 << 16);
   }
 
   // ---- V (no RoPE): rotated like K unless TQ_V_ROTATE is off. The V loads
@@ -444,26 +470,35 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   if (!rotated && (a.flags & kVRotate)) {
     rotate_tokens<F16>(x, a, a.v, s_pih, s_pil, li, b, h, j0, lane, false);
   } else {
+    const int jl = j0 + lane;
+    const bool okl = ok_of(jl);
+    const int64_t row = row_of(jl);
 #pragma unroll
-    for (int i = 0; i < kDim; ++i) x[i] = ok ? load_in(a.v, row + i, F16) : 0.0f;
+    for (int i = 0; i < kDim; ++i) x[i] = okl ? load_in(a.v, row + i, F16) : 0.0f;
   }
   uint32_t vw[8];
   const QuantOut qv = quantize_lane<false>(x, Lv, s_lev[1], nullptr, (VQJL && !paper) ? 3 : vsign, vw);
-  if (VQJL && !paper) {
-    const uint64_t sb = projected_signs(x, qv.g, s_sh, s_sl, s_Sn, a.qjl_s, lane);
-#pragma unroll
-    for (int i = 0; i < kDim; ++i) vw[i >> 3] |= (uint32_t)((sb >> i) & 1ull) << (4 * (i & 7) + 3);
-  }
-  if (ok) {
-    *reinterpret_cast<uint2*>(a.scalars + (lh * a.slots + slot) * 4) =
-        make_uint2(qk.n16 | (qk.g16 << 16), qv.n16 | (qv.g16 << 16));
-  }
-
   // V is stored dimension-major: transpose the wave's 64 x 64 nibbles through
-  // its LDS buffer (token-major words in, one dimension per lane out).
+  // its LDS buffer (token-major words in, one dimension per lane out). The
+  // words go there first; the projected signs of the value residual, where
+  // asked for, are merged in there (registers).
   uint32_t* s_w = s_vt[wave];
 #pragma unroll
   for (int w = 0; w < 8; ++w) s_w[lane * 8 + w] = vw[w];
+  if (VQJL && !paper) {
+    const uint64_t sb = projected_signs(x, qv.g, s_sh, s_sl, s_Sn, a.qjl_s, lane);
+    const int lv = lane_of();
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      uint32_t add = 0;
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) add |= (uint32_t)((sb >> (8 * w + jj)) & 1ull) << (4 * jj + 3);
+      s_w[lv * 8 + w] |= add;
+    }
+  }
+  const int jv = j0 + lane_of();
+  const bool ok = ok_of(jv);
+  if (ok) reinterpret_cast<uint32_t*>(a.scalars + (lh * a.slots + sbase + jv) * 4)[1] = qv.n16 | (qv.g16 << 16);
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
