@@ -42,8 +42,6 @@
 //             sign bits.
 // Work items are dealt so that all splits of a unit land on one XCD (blocks
 // go to the 8 XCDs round-robin), where Pi stays in that XCD's L2.
-#include <atomic>
-
 #include "tq_append.hpp"
 #include "tq_device.hpp"
 #include "tq_internal.hpp"
@@ -496,11 +494,8 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 
   // Wave priority: the prologue, and the merge and epilogue after the tile
   // loop, are chains that gate a block's tile requests or its end; they issue
-  // ahead of the other blocks' tile loops on the same SIMD (3 blocks per
-  // compute unit, up to 6 waves per SIMD). Among tile loops, a block started
-  // in a later layer of the launch (one block per compute unit per layer)
-  // issues ahead of earlier ones, so the blocks of a compute unit end closer
-  // together.
+  // ahead of the tile loops of the other blocks on the same SIMD (3 blocks per
+  // compute unit, up to 6 waves per SIMD), which are throughput work.
   __builtin_amdgcn_s_setprio(3);
   // -------------------------------------------------------------- prologue
   // q' = RoPE(q) (wave 0, one element per lane), then q^ = Pi q' and u = S q^
@@ -623,15 +618,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
   }
 
-  {
-    const int layer = bid / (a.layer_blocks > 0 ? a.layer_blocks : 256);
-    if (layer >= 2)
-      __builtin_amdgcn_s_setprio(2);
-    else if (layer == 1)
-      __builtin_amdgcn_s_setprio(1);
-    else
-      __builtin_amdgcn_s_setprio(0);
-  }
+  __builtin_amdgcn_s_setprio(0);
   // -------------------------------------------------------------- main loop
   float m_run = -INFINITY;
   float l_lane = 0.0f;
@@ -901,23 +888,7 @@ void decode_plan(int units, int max_len, int* waves, int* nsplit, int* split_til
   *nsplit = (ntiles + st - 1) / st;
 }
 
-// Compute units of the current device (queried once per device; 0 if the
-// query fails, which leaves the kernel's default of 256).
-static int compute_units() {
-  static std::atomic<int> cached[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-  int n = cached[dev].load(std::memory_order_relaxed);
-  if (n == 0) {
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    cached[dev].store(n, std::memory_order_relaxed);
-  }
-  return n;
-}
-
-hipError_t launch_decode(const DecodeArgs& args, int waves, hipStream_t st) {
-  DecodeArgs a = args;
-  a.layer_blocks = compute_units();
+hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st) {
   const int64_t units = (int64_t)a.nlayers * a.B * a.H;
   const int64_t total = units * a.nsplit;
   const int64_t per_xcd = (total + kXcds - 1) / kXcds;

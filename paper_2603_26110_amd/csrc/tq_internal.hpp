@@ -63,8 +63,6 @@ struct DecodeArgs {
   int append;
   int len_add;
   int wait_limit;          // polls of a decode step's wait for its appends before giving up
-  int layer_blocks;        // blocks the GPU starts at once (one per compute unit); the tile loop of
-                           // blocks started in later layers runs at a higher wave priority
 };
 
 // Default bound of that wait (never reached: the appends wait on nothing).
