@@ -225,6 +225,10 @@ tq_status decode_common(const tq_params* params, const tq_cache* cache, const vo
   a.nsplit = nsplit; a.split_tiles = split_tiles;
   a.k_new = k; a.v_new = v; a.append = step ? 1 : 0; a.len_add = step ? 1 : 0;
   a.wait_limit = g_wait_limit.load(std::memory_order_relaxed);
+  a.div_ns = tq::make_div_magic((uint32_t)nsplit);
+  a.div_h = tq::make_div_magic((uint32_t)a.H);
+  a.div_b = tq::make_div_magic((uint32_t)B);
+  a.div_st = tq::make_div_magic((uint32_t)split_tiles);
   char* ws = (char*)workspace;
   if (nsplit > 1) {
     a.partials = (float*)ws;

@@ -22,9 +22,14 @@
 //   step      for a decode step (quantize-then-attend) waves 1 and 2 then
 //             quantize the new key and value into the cache with the append
 //             kernel's wave-per-vector quantizer on the staged Pi and S, while
-//             the other waves score; the wave that scores the new token's
-//             tile waits for them and substitutes the new codes in the
-//             registers of that tile (loaded before the append wrote them).
+//             the other waves score.
+//   last token the tiles cover tokens 0 .. n-2; token n-1 (a step's new one)
+//             is scored on its own by wave 3 after its tiles, from the
+//             append's codes in LDS (a step) or from registers loaded with
+//             its first tile (an attend). With 1024 cached tokens and one new
+//             one every wave then takes two tiles, where a 17th one-token
+//             tile would cost one wave a third round trip and a full tile of
+//             work.
 //   main loop keys are scored one lane per token from the key words (3-bit
 //             indices in bits 0-23, signs in bits 24-31):
 //             score = n_k/8 (sum T_A + coef sum T_B), coef = alpha g_k (QJL) or
@@ -305,37 +310,14 @@ struct Lut8 {
 };
 
 
-// The appended token's codes as the append wrote them into LDS
-// (s_new = [n_k | g_k, n_v | g_v], key words 0..7, value nibbles of
-// dimensions 0..63) replace row `row` of a tile loaded before the append:
-// the key words and scalars of lane `row`, and in every lane (a dimension)
-// the row's nibble of the value word of its 8-token group.
-__device__ __forceinline__ void patch_new_token(TileRegs& r, const uint32_t* s_new, int row, int lane) {
-  const bool mine = lane == row;
-  const uint4 k0 = make_uint4(s_new[2], s_new[3], s_new[4], s_new[5]);
-  const uint4 k1 = make_uint4(s_new[6], s_new[7], s_new[8], s_new[9]);
-  const uint32_t sk = s_new[0], sv = s_new[1];
-  r.k0.x = mine ? k0.x : r.k0.x; r.k0.y = mine ? k0.y : r.k0.y;
-  r.k0.z = mine ? k0.z : r.k0.z; r.k0.w = mine ? k0.w : r.k0.w;
-  r.k1.x = mine ? k1.x : r.k1.x; r.k1.y = mine ? k1.y : r.k1.y;
-  r.k1.z = mine ? k1.z : r.k1.z; r.k1.w = mine ? k1.w : r.k1.w;
-  r.sc.x = mine ? sk : r.sc.x;
-  r.sc.y = mine ? sv : r.sc.y;
-  const uint32_t sh = 4u * (uint32_t)(row & 7);
-  const uint32_t nib = s_new[10 + lane] << sh, keep = ~(15u << sh);
-  uint4& v = (row < 32) ? r.v0 : r.v1;   // row is wave-uniform
-  switch ((row & 31) >> 3) {
-    case 0: v.x = (v.x & keep) | nib; break;
-    case 1: v.y = (v.y & keep) | nib; break;
-    case 2: v.z = (v.z & keep) | nib; break;
-    default: v.w = (v.w & keep) | nib; break;
-  }
-}
-
 template <int WAVES, bool VQJL>
 __global__ __launch_bounds__(WAVES * 64)
 __attribute__((amdgpu_waves_per_eu((WAVES == 8 && !VQJL) ? 6 : 1)))
 void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
+  // Wave priority 3 from the start: the block's first steps (its indices and
+  // the request of Pi) issue ahead of the tile loops of blocks already
+  // running on the SIMD.
+  __builtin_amdgcn_s_setprio(3);
   constexpr int NT = WAVES * 64;
   constexpr int TAM = 2048 / NT;           // pair-table entries per thread
   constexpr int TBM = 512 / NT;            // groups of 4 sign-table entries per thread
@@ -382,11 +364,15 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   const int bid = blockIdx.x;
   const int work = (bid % kXcds) * per_xcd + bid / kXcds;
   if (work >= total_work) return;
-  const int unit = work / nsplit;
+  // The unit's indices by multiply-high divisions on the scalar unit (an
+  // integer division the compiler would expand on the vector unit).
+  const int unit = (int)div_magic(work, a.div_ns);
   const int split = work - unit * nsplit;
-  const int h = unit % H;
-  const int b = (unit / H) % B;
-  const int l = layer0 + unit / (H * B);
+  const int uh = (int)div_magic(unit, a.div_h);
+  const int h = unit - uh * H;
+  const int ub = (int)div_magic(uh, a.div_b);
+  const int b = uh - ub * B;
+  const int l = layer0 + ub;
   const int lh = l * H + h;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
@@ -476,10 +462,15 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     return;
   }
   const int tile_end = min(ntiles, tile_begin + a.split_tiles);
-  const int participants = (ntiles + a.split_tiles - 1) / a.split_tiles;
-  // a step's new token (index n - 1) is appended by the block of its tile
+  const int participants = (int)div_magic(ntiles + a.split_tiles - 1, a.div_st);
+  // Token n - 1 (a step's new one, appended by the block of its tile) is
+  // scored on its own by the last wave of that block; the tile loop covers
+  // the other n - 1 tokens.
   const int tnew = (n - 1) >> 6, rnew = (n - 1) & 63;
-  const bool app = step && tnew >= tile_begin && tnew < tile_end;
+  const bool own_last = tnew >= tile_begin && tnew < tile_end;
+  const bool app = step && own_last;
+  const int nm = n - 1;
+  const int tile_end_main = min(tile_end, (nm + 63) >> 6);
 
   const uint8_t* kreg = a.k_codes + (int64_t)lh * a.slots * 32;
   const uint8_t* vreg = a.v_codes + (int64_t)lh * a.slots * 32;
@@ -492,11 +483,11 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   __builtin_amdgcn_s_waitcnt(0x0F70);      // vmcnt(0)
   lds_barrier();
 
-  // Wave priority: the prologue, and the merge and epilogue after the tile
-  // loop, are chains that gate a block's tile requests or its end; they issue
-  // ahead of the tile loops of the other blocks on the same SIMD (3 blocks per
-  // compute unit, up to 6 waves per SIMD), which are throughput work.
-  __builtin_amdgcn_s_setprio(3);
+  // (Wave priority: the start of the block and the prologue, and the merge
+  // and epilogue after the tile loop, are chains that gate a block's tile
+  // requests or its end; at priority 3 they issue ahead of the tile loops of
+  // the other blocks on the same SIMD (3 blocks per compute unit, up to 6
+  // waves per SIMD), which are throughput work and run at 0.)
   // -------------------------------------------------------------- prologue
   // q' = RoPE(q) (wave 0, one element per lane), then q^ = Pi q' and u = S q^
   // by all waves: 8 lanes per row, 8 columns each, summed by DPP.
@@ -579,8 +570,8 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   // For a decode step, waves 1 and 2 quantize the new key and value into the
   // cache (with the append kernel's quantizer, on the staged Pi and S) while
   // the other waves start scoring; each raises the count in s_ready when its
-  // codes are in s_new. The wave that scores the new token's tile waits for
-  // both before it does (bounded: the appends never wait on anything).
+  // codes are in s_new. Wave 3 waits for both before it scores the new token
+  // after its tiles (bounded: the appends never wait on anything).
   if (app && (wave == 1 || wave == 2)) {
     const bool is_v = wave == 2;
     const int ksign = paper ? 2 : 1;
@@ -612,10 +603,29 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   // Tiles are requested only now (the appending waves' registers hold no
   // tiles through the append).
   TileRegs buf[DEPTH];
+  if (tile_end_main > tile_begin) {
 #pragma unroll
-  for (int d = 0; d < DEPTH; ++d) {
-    const int tq = min(tile_begin + wave + d * WAVES, tile_end - 1);   // (a wave without tiles re-reads one)
-    load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
+    for (int d = 0; d < DEPTH; ++d) {
+      const int tq = min(tile_begin + wave + d * WAVES, tile_end_main - 1);   // (a wave without tiles re-reads one)
+      load_tile(buf[d], kreg, vreg, sreg, tile0 + tq, s0, tq, lane);
+    }
+  }
+  // An attend's last token: its key words and scalars (every lane the same
+  // address) and, per lane, the value word of its dimension that holds the
+  // token's nibble, requested after the first tile. (A copy straight into
+  // LDS would make the compiler wait for every load before each tile's first
+  // LDS read, which stops it from scoring a tile's keys while its values are
+  // still arriving.) Wave 3 scores it: it does not append, and with
+  // WAVES = 4 it has no more tiles than any other wave.
+  const bool lone = own_last && wave == 3;
+  TileRegs last{};
+  if (lone && !step) {
+    const int64_t gt = tile0 + tnew;
+    last.k0 = *reinterpret_cast<const uint4*>(kreg + tile_half_offset(gt, 0, rnew));
+    last.k1 = *reinterpret_cast<const uint4*>(kreg + tile_half_offset(gt, 1, rnew));
+    last.sc = sreg[s0 + nm];
+    last.v0.x = *reinterpret_cast<const uint32_t*>(vreg + tile_half_offset(gt, rnew >> 5, lane) +
+                                                   4 * ((rnew & 31) >> 3));
   }
 
   __builtin_amdgcn_s_setprio(0);
@@ -627,29 +637,14 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   const float lscale = a.logit_scale2;
   const char* vtab = reinterpret_cast<const char*>(s_vtab);
 
-  for (int tb = tile_begin + wave; tb < tile_end; tb += DEPTH * WAVES) {
+  for (int tb = tile_begin + wave; tb < tile_end_main; tb += DEPTH * WAVES) {
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) {
       const int tt = tb + d * WAVES;
-      if (tt >= tile_end) break;
-      if (app && tt == tnew) {
-        // bounded wait for the two appends; if it gives up, the unit's
-        // output is marked NaN (s_fail) instead of scoring stale codes
-        bool got = false;
-        for (int i = 0; i < a.wait_limit; ++i) {
-          if (__hip_atomic_load(&s_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= 2) {
-            got = true;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-        }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-        if (!got && lane == 0) s_fail = 1;
-        patch_new_token(buf[d], s_new, rnew, lane);
-      }
+      if (tt >= tile_end_main) break;
       const TileRegs& cur = buf[d];
       const int tok = tt * kTile + lane;
-      const bool tv = tok < n;
+      const bool tv = tok < nm;
       // ---- key score, one lane per token: per key word 4 pair-table reads
       // (table term) and 1 sign-table read (QJL term). The empty asm pins the
       // partial sums half way so the compiler does not hoist every table read
@@ -703,12 +698,74 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
         value_sign_word<6>(tg, vw[6], sg);
         value_sign_word<7>(tg, vw[7], sg);
       }
-        const int tn = tt + DEPTH * WAVES;
-        if (tn < tile_end) load_tile(buf[d], kreg, vreg, sreg, tile0 + tn, s0, tn, lane);
+      const int tn = tt + DEPTH * WAVES;
+      if (tn < tile_end_main) load_tile(buf[d], kreg, vreg, sreg, tile0 + tn, s0, tn, lane);
     }
   }
 
   __builtin_amdgcn_s_setprio(3);
+  // ------------------------------------------------------------ last token
+  // Scored with the tile loop's arithmetic (every lane computes the same
+  // logit); its value enters lane d's accumulator through dimension d's code.
+  if (lone) {
+    // key words 0..7 and scalars of the token, and this lane's nibble
+    const uint32_t* tok_k;
+    uint2 sc;
+    uint32_t nib;
+    if (step) {
+      // bounded wait for the two appends; if it gives up, the unit's output
+      // is marked NaN (s_fail) instead of scoring stale codes
+      bool got = false;
+      for (int i = 0; i < a.wait_limit; ++i) {
+        if (__hip_atomic_load(&s_ready, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) >= 2) {
+          got = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+      if (!got && lane == 0) s_fail = 1;
+      tok_k = s_new + 2;
+      sc = make_uint2(s_new[0], s_new[1]);
+      nib = s_new[10 + lane] & 15u;
+    } else {
+      tok_k = nullptr;
+      sc = last.sc;
+      nib = (last.v0.x >> (4 * (rnew & 7))) & 15u;
+    }
+    if (step) {
+      last.k0 = make_uint4(tok_k[0], tok_k[1], tok_k[2], tok_k[3]);
+      last.k1 = make_uint4(tok_k[4], tok_k[5], tok_k[6], tok_k[7]);
+    }
+    float A = 0.0f, B = 0.0f;
+    key_word_score<0>(s_ta, s_tb, last.k0.x, A, B);
+    key_word_score<1>(s_ta, s_tb, last.k0.y, A, B);
+    key_word_score<2>(s_ta, s_tb, last.k0.z, A, B);
+    key_word_score<3>(s_ta, s_tb, last.k0.w, A, B);
+    key_word_score<4>(s_ta, s_tb, last.k1.x, A, B);
+    key_word_score<5>(s_ta, s_tb, last.k1.y, A, B);
+    key_word_score<6>(s_ta, s_tb, last.k1.z, A, B);
+    key_word_score<7>(s_ta, s_tb, last.k1.w, A, B);
+    const float nk = half_bits_to_float(sc.x), gk = half_bits_to_float(sc.x >> 16);
+    const float nv = half_bits_to_float(sc.y), gv = half_bits_to_float(sc.y >> 16);
+    const float coef = paper ? ebar_k : kQjlAlpha * gk;
+    const float lg = nk * lscale * fmaf(coef, B, A);
+    if (lg > m_run + kLazyRescale) {
+      const float f = __builtin_amdgcn_exp2f(m_run - lg);
+      l_lane *= f;
+      sg *= f;
+      o0 *= f; o1 *= f; o2 *= f; o3 *= f;
+      m_run = lg;
+    }
+    const float p = __builtin_amdgcn_exp2f(lg - m_run);
+    if (lane == 0) l_lane += p;
+    const float wv = p * nv * 0.125f;
+    o0 = fmaf(wv, s_vtab[nib], o0);
+    if (VQJL) {
+      const float wg = paper ? wv : wv * gv;
+      sg = fmaf(wg, (nib & 8u) ? 1.0f : -1.0f, sg);
+    }
+  }
   // ------------------------------------------------------ merge the waves
   // (s_wo shares its LDS with S, which a step's key append may still be
   // reading until every wave has come here)

@@ -28,6 +28,27 @@ struct QuantArgs {
   int64_t slots;
 };
 
+// Division of a nonnegative n < 2^31 by a fixed d >= 1 as
+//   q = (umulhi(n, m) + n) >> s,  s = ceil(log2 d),  m = floor(2^32 (2^s - d) / d) + 1
+// (the round-up method with a 33-bit multiplier 2^32 + m; umulhi(n, m) + n
+// stays below 2^32 for n < 2^31). With d, m and s kernel arguments the
+// division runs on the scalar unit.
+struct DivMagic {
+  uint32_t m;
+  uint32_t s;
+};
+
+inline DivMagic make_div_magic(uint32_t d) {
+  uint32_t s = 0;
+  while ((uint64_t(1) << s) < d) ++s;
+  const uint64_t m = ((uint64_t(1) << 32) * ((uint64_t(1) << s) - d)) / d + 1;
+  return DivMagic{(uint32_t)m, s};
+}
+
+__device__ __forceinline__ uint32_t div_magic(int n, DivMagic d) {
+  return (__umulhi((uint32_t)n, d.m) + (uint32_t)n) >> d.s;
+}
+
 struct DecodeArgs {
   const void* q;
   int B, H, layer0, nlayers;
@@ -63,6 +84,7 @@ struct DecodeArgs {
   int append;
   int len_add;
   int wait_limit;          // polls of a decode step's wait for its appends before giving up
+  DivMagic div_ns, div_h, div_b, div_st;   // by nsplit, H, B and split_tiles
 };
 
 // Default bound of that wait (never reached: the appends wait on nothing).
