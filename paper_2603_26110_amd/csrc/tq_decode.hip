@@ -289,23 +289,13 @@ __device__ __forceinline__ float2 pair_f2(uint64_t w) {
   return make_float2(__uint_as_float((uint32_t)w), __uint_as_float((uint32_t)(w >> 32)));
 }
 
-// Eight table levels held in (scalar) registers; pick() selects one per lane
-// by three levels of selects on the index bits, never through memory.
+// Eight table levels held in (scalar) registers, for a step's appends (their
+// quantizer compares against them and their midpoints as scalar operands).
 struct Lut8 {
   float c0, c1, c2, c3, c4, c5, c6, c7;
   __device__ __forceinline__ static Lut8 of(const uint64_t (&w)[4]) {
     const float2 a = pair_f2(w[0]), b = pair_f2(w[1]), c = pair_f2(w[2]), d = pair_f2(w[3]);
     return Lut8{a.x, a.y, b.x, b.y, c.x, c.y, d.x, d.y};
-  }
-  // strictly ascending (false for any NaN level)
-  __device__ __forceinline__ bool ascending() const {
-    return (c0 < c1) & (c1 < c2) & (c2 < c3) & (c3 < c4) & (c4 < c5) & (c5 < c6) & (c6 < c7);
-  }
-  __device__ __forceinline__ float pick(int i) const {
-    const bool b0 = (i & 1) != 0, b1 = (i & 2) != 0, b2 = (i & 4) != 0;
-    const float p01 = b0 ? c1 : c0, p23 = b0 ? c3 : c2, p45 = b0 ? c5 : c4, p67 = b0 ? c7 : c6;
-    const float p03 = b1 ? p23 : p01, p47 = b1 ? p67 : p45;
-    return b2 ? p47 : p03;
   }
 };
 
@@ -441,13 +431,23 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     const int qpc = min(max(qp, 0), rope_positions - 1);
     cs = reinterpret_cast<const float2*>(rope_cs + (int64_t)qpc * 2 * kPairs)[half ? (lane & 31) : (lane >> 1)];
   }
+  // Per lane, the levels the tables are built from: c_K[lane & 7],
+  // c_K[lane >> 3] and c_V[lane & 7] (vector loads: a per-lane choice among
+  // eight scalar values would take seven selects each).
+  const float lev_k_lo = lut_k[lh * 8 + (lane & 7)];
+  const float lev_k_hi = lut_k[lh * 8 + (lane >> 3)];
+  const float lev_v = lut_v[lh * 8 + (lane & 7)];
   const Lut8 ck = Lut8::of(kw), cvl = Lut8::of(vw);
   const float ebar_k = paper ? ebar_raw : 0.0f;
   const int n = len + len_add;             // tokens attended (the step's new one included)
   // a unit whose sequence range or query position is out of bounds, or
   // whose K or V table is not strictly ascending, is not appended to and
-  // gets NaN output
-  const bool asc = ck.ascending() && cvl.ascending();
+  // gets NaN output. Lanes 0..6 compare their level with the next one (a
+  // NaN level fails).
+  const float next_k = dpp<0x101>(lev_k_lo);   // row_shl:1: lane i + 1
+  const float next_v = dpp<0x101>(lev_v);
+  const bool lane_asc = (lane & 7) == 7 || (lev_k_lo < next_k && lev_v < next_v);
+  const bool asc = (__builtin_amdgcn_ballot_w64(!lane_asc) & 0xFFull) == 0;
   const bool valid = (n >= 0) & (n <= a.max_len) & (s0 >= 0) & ((s0 & 63) == 0) &
                      (s0 + n <= a.slots) & (qp >= 0) & (qp < rope_positions) & asc;
   if (!valid || n == 0) {
@@ -540,7 +540,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   //   tb (2048 entries in groups of 4): group e = t + NT m of word w = e / 64,
   //      sign bytes 4 (e % 64) .. 4 (e % 64) + 3
   {
-    const float ck_lo = ck.pick(lane & 7), ck_hi = ck.pick(lane >> 3);
+    const float ck_lo = lev_k_lo, ck_hi = lev_k_hi;
 #pragma unroll
     for (int m = 0; m < TAM; ++m) {
       const float2 qq = reinterpret_cast<const float2*>(s_vec[1])[wave + WAVES * m];
@@ -562,7 +562,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
       v.w = (base + u[0]) + u[1];
       reinterpret_cast<float4*>(s_tb)[e] = v;
     }
-    s_vtab[t & 15] = cvl.pick(t & 7);   // every thread: identical values
+    if (t < 16) s_vtab[t] = lev_v;       // c_V[t & 7]
   }
   lds_barrier();
 
@@ -665,9 +665,10 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
       float lg = nk * lscale * fmaf(coef, B, A);
       lg = tv ? lg : -INFINITY;
 
-      // ---- online softmax (base 2), lazily rescaled
-      const float tmax = wave_max_uniform(lg);
-      if (tmax > m_run + kLazyRescale) {
+      // ---- online softmax (base 2), lazily rescaled: the tile max is formed
+      // only when some lane exceeds the running max by the headroom
+      if (__builtin_amdgcn_ballot_w64(lg > m_run + kLazyRescale) != 0) {
+        const float tmax = wave_max_uniform(lg);
         const float f = __builtin_amdgcn_exp2f(m_run - tmax);
         l_lane *= f;
         sg *= f;
