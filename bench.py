@@ -527,6 +527,7 @@ def workload_line(torch, tq, synth, name, replays, cpu_seconds, eager=False, cpu
     same = bool(np.all(lens == lens[0]))
     bidx = torch.arange(B, device=dev)
     lens_d = t_(lens.astype(np.int64))
+    tokens_d = t_(lens.astype(np.int32))
     pf_ms = 0.0
     for l in range(L):
         gen = synth.device_generator(wl.seed, l, dev)
@@ -537,20 +538,13 @@ def workload_line(torch, tq, synth, name, replays, cpu_seconds, eager=False, cpu
             k_all[s, l] = kl[bidx, lens_d + s]
             v_all[s, l] = vl[bidx, lens_d + s]
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        if same:
-            kp, vp = kl[None, :, :tmax].contiguous(), vl[None, :, :tmax].contiguous()
-            e0.record()
-            tq.quantize_pack(params, cache, kp, vp, t_(np.zeros(B, np.int32)), offs_d, pi_d, lk_d, lv_d, S_d,
-                             layer0=l)
-            e1.record()
-        else:
-            parts = [(kl[b:b + 1, :int(lens[b])][None].contiguous(), vl[b:b + 1, :int(lens[b])][None].contiguous())
-                     for b in range(B)]
-            e0.record()
-            for b, (kp, vp) in enumerate(parts):
-                tq.quantize_pack(params, cache, kp, vp, t_(np.zeros(1, np.int32)), offs_d[b:b + 1], pi_d, lk_d,
-                                 lv_d, S_d, layer0=l)
-            e1.record()
+        # one call per layer; a ragged batch passes each sequence's length
+        # (its rows past that length are padding, not read)
+        kp, vp = kl[None, :, :tmax].contiguous(), vl[None, :, :tmax].contiguous()
+        e0.record()
+        tq.quantize_pack(params, cache, kp, vp, t_(np.zeros(B, np.int32)), offs_d, pi_d, lk_d, lv_d, S_d,
+                         layer0=l, seq_tokens=None if same else tokens_d)
+        e1.record()
         torch.cuda.synchronize()
         pf_ms += e0.elapsed_time(e1)
         del kl, vl

@@ -12,7 +12,8 @@
  *   decode   (Sec. 3.1 decode steps 1-4, Algorithm 1 of Sec. 4.3):
  *       one pass over the packed cache: dequantize through the tables in
  *       registers, add the QJL score correction, online softmax, accumulate V.
- * Entry points: tq_quantize_pack (prefill and appends), tq_decode_attend,
+ * Entry points: tq_quantize_pack (prefill and appends) and
+ * tq_quantize_pack_ragged (a prefill of sequences of different lengths), tq_decode_attend,
  * tq_decode_step (append + attend in one launch), tq_dequantize (fp16 rows
  * for a dequantize-then-attend path), tq_calibrate_rotation and
  * tq_calibrate_lut (Sec. 3.2-3.3), tq_calibrate_ebar (Sec. 3.4), tq_rope_table
@@ -178,6 +179,24 @@ TQ_API tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache
                            const int32_t* pos0, const int64_t* slot0,
                            const float* pi, const float* lut_k, const float* lut_v,
                            const float* qjl_s, const float* ebar, void* stream);
+
+/* tq_quantize_pack for a batch of sequences of different lengths (the same
+ * steps, Sec. 3.1 prefill steps 1, 3, 4), in one call: sequence b has
+ *   T_b = min(max(seq_tokens[b], 0), T)
+ * tokens, j < T_b; rows j >= T_b of its input are padding and no slot is
+ * written for them. Every token gets the bytes tq_quantize_pack gives it.
+ *   seq_tokens  device int32 [B] (required).
+ *   k, v        device [nlayers][B][T][H][64] as for tq_quantize_pack (T is
+ *               the longest sequence; padding rows need not be initialized).
+ * Other arguments and errors as for tq_quantize_pack; a NULL seq_tokens is
+ * TQ_ERR_ARG. */
+TQ_API tq_status tq_quantize_pack_ragged(const tq_params* params, const tq_cache* cache,
+                                  const void* k, const void* v,
+                                  int32_t B, int32_t T, const int32_t* seq_tokens,
+                                  int32_t layer0, int32_t nlayers,
+                                  const int32_t* pos0, const int64_t* slot0,
+                                  const float* pi, const float* lut_k, const float* lut_v,
+                                  const float* qjl_s, const float* ebar, void* stream);
 
 /* Fused decode attention over the packed cache (Sec. 3.1 decode steps 1-4;
  * Algorithm 1 of Sec. 4.3; the query is rotated once instead of rotating

@@ -69,6 +69,8 @@ def _load():
     L.tq_rope_table.restype = i32
     L.tq_quantize_pack.argtypes = [P, P, P, P, i32, i32, i32, i32, P, P, P, P, P, P, P, P]
     L.tq_quantize_pack.restype = i32
+    L.tq_quantize_pack_ragged.argtypes = [P, P, P, P, i32, i32, P, i32, i32, P, P, P, P, P, P, P, P]
+    L.tq_quantize_pack_ragged.restype = i32
     L.tq_decode_attend.argtypes = [P, P, P, i32, i32, i32, P, P, P, i32, P, P, P, P, P, P, P, sz, P]
     L.tq_decode_attend.restype = i32
     L.tq_decode_step.argtypes = [P, P, P, P, P, i32, i32, i32, P, P, P, i32, P, P, P, P, P, P, P, sz, P]
@@ -171,8 +173,10 @@ def rope_table(positions: int, base: float = 10000.0, device="cuda") -> torch.Te
 
 
 def quantize_pack(params: Params, cache: Cache, k, v, pos0, slot0, pi, lut_k, lut_v, qjl_s,
-                  ebar=None, layer0: int = 0) -> None:
-    """k, v: [nlayers][B][T][H][64] (params.io_dtype; fp32 with INPUT_ROTATED)."""
+                  ebar=None, layer0: int = 0, seq_tokens=None) -> None:
+    """k, v: [nlayers][B][T][H][64] (params.io_dtype; fp32 with INPUT_ROTATED).
+    seq_tokens (int32 [B], optional): each sequence's token count for a
+    ragged batch (tq_quantize_pack_ragged); rows beyond it are padding."""
     L = _load()
     want = torch.float32 if params.flags & INPUT_ROTATED else params.io_dtype
     _dev(k, "k", want)
@@ -188,6 +192,15 @@ def quantize_pack(params: Params, cache: Cache, k, v, pos0, slot0, pi, lut_k, lu
         _dev(t, name, torch.float32)
     p = params.c()
     c = cache.c()
+    if seq_tokens is not None:
+        _dev(seq_tokens, "seq_tokens", torch.int32)
+        if seq_tokens.numel() < B:
+            raise ValueError("seq_tokens needs B entries")
+        _check(L.tq_quantize_pack_ragged(ctypes.byref(p), ctypes.byref(c), _ptr(k), _ptr(v), B, T,
+                                         _ptr(seq_tokens), layer0, nl, _ptr(pos0), _ptr(slot0), _ptr(pi),
+                                         _ptr(lut_k), _ptr(lut_v), _ptr(qjl_s), _ptr(ebar),
+                                         _stream(k.device)))
+        return
     _check(L.tq_quantize_pack(ctypes.byref(p), ctypes.byref(c), _ptr(k), _ptr(v), B, T, layer0, nl,
                               _ptr(pos0), _ptr(slot0), _ptr(pi), _ptr(lut_k), _ptr(lut_v),
                               _ptr(qjl_s), _ptr(ebar), _stream(k.device)))

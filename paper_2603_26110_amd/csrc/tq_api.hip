@@ -120,12 +120,16 @@ tq_status tq_rope_table(float* cs, int32_t positions, double base, void* stream)
   return hip_status(tq::launch_rope_table(cs, positions, base, (hipStream_t)stream), "tq_rope_table launch");
 }
 
-tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache, const void* k,
-                           const void* v, int32_t B, int32_t T, int32_t layer0, int32_t nlayers,
-                           const int32_t* pos0, const int64_t* slot0, const float* pi,
-                           const float* lut_k, const float* lut_v, const float* qjl_s,
-                           const float* ebar, void* stream) {
-  (void)ebar;
+}  // extern "C"
+
+namespace {
+
+// Shared by tq_quantize_pack and tq_quantize_pack_ragged (seq_tokens
+// non-NULL: sequence b has its own token count).
+tq_status quantize_common(const tq_params* params, const tq_cache* cache, const void* k, const void* v,
+                          int32_t B, int32_t T, const int32_t* seq_tokens, int32_t layer0, int32_t nlayers,
+                          const int32_t* pos0, const int64_t* slot0, const float* pi, const float* lut_k,
+                          const float* lut_v, const float* qjl_s, void* stream) {
   const bool rotated = params && (params->flags & TQ_INPUT_ROTATED);
   tq_status s = check_params(params, !rotated);
   if (s != TQ_OK) return s;
@@ -153,7 +157,34 @@ tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache, const
   a.pos0 = pos0; a.slot0 = slot0; a.pi = pi; a.lut_k = lut_k; a.lut_v = lut_v; a.qjl_s = qjl_s;
   a.k_codes = (uint8_t*)cache->k_codes; a.v_codes = (uint8_t*)cache->v_codes;
   a.scalars = (uint16_t*)cache->scalars; a.slots = cache->slots;
-  return hip_status(tq::launch_quantize(a, (hipStream_t)stream), "tq_quantize_pack launch");
+  a.tokens = seq_tokens;
+  return hip_status(tq::launch_quantize(a, (hipStream_t)stream),
+                    seq_tokens ? "tq_quantize_pack_ragged launch" : "tq_quantize_pack launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+tq_status tq_quantize_pack(const tq_params* params, const tq_cache* cache, const void* k,
+                           const void* v, int32_t B, int32_t T, int32_t layer0, int32_t nlayers,
+                           const int32_t* pos0, const int64_t* slot0, const float* pi,
+                           const float* lut_k, const float* lut_v, const float* qjl_s,
+                           const float* ebar, void* stream) {
+  (void)ebar;
+  return quantize_common(params, cache, k, v, B, T, nullptr, layer0, nlayers, pos0, slot0, pi, lut_k, lut_v,
+                         qjl_s, stream);
+}
+
+tq_status tq_quantize_pack_ragged(const tq_params* params, const tq_cache* cache, const void* k,
+                                  const void* v, int32_t B, int32_t T, const int32_t* seq_tokens,
+                                  int32_t layer0, int32_t nlayers, const int32_t* pos0,
+                                  const int64_t* slot0, const float* pi, const float* lut_k,
+                                  const float* lut_v, const float* qjl_s, const float* ebar, void* stream) {
+  (void)ebar;
+  if (!seq_tokens && (int64_t)B * T * nlayers != 0) return fail(TQ_ERR_ARG, "seq_tokens is NULL");
+  return quantize_common(params, cache, k, v, B, T, seq_tokens, layer0, nlayers, pos0, slot0, pi, lut_k,
+                         lut_v, qjl_s, stream);
 }
 
 size_t tq_decode_workspace_bytes(const tq_params* params, int32_t B, int32_t nlayers, int32_t max_len) {

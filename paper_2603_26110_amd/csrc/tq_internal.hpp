@@ -26,6 +26,7 @@ struct QuantArgs {
   uint8_t* v_codes;
   uint16_t* scalars;
   int64_t slots;
+  const int32_t* tokens;   // [B] tokens of each sequence (<= T), or null: all T
 };
 
 // Division of a nonnegative n < 2^31 by a fixed d >= 1 as

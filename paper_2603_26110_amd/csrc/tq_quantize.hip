@@ -137,7 +137,7 @@ __device__ __forceinline__ void to_lane_per_token(f32x16 (&acc)[2][2], float (&o
 // lane's token scale (of token j0 + lane, for scaling the result back).
 template <bool F16>
 __device__ __forceinline__ float load_split_rows(SplitOps& ops, const QuantArgs& a, const void* src, int li,
-                                                 int b, int h, int j0, int lane, bool rope) {
+                                                 int b, int h, int j0, int Tb, int lane, bool rope) {
   const int n = lane & 31, hh = lane >> 5;
   const bool half = (a.flags & kRopeHalf) != 0;
   float sc_nb[2];
@@ -145,7 +145,7 @@ __device__ __forceinline__ float load_split_rows(SplitOps& ops, const QuantArgs&
   for (int nb = 0; nb < 2; ++nb) {
     const int j = j0 + 32 * nb + n;
     const int pos = a.pos0[b] + j;
-    const bool ok = j < a.T && (!rope || (pos >= 0 && pos < a.rope_positions));
+    const bool ok = j < Tb && (!rope || (pos >= 0 && pos < a.rope_positions));
     const int64_t row = ((((int64_t)li * a.B + b) * a.T + j) * a.H + h) * kDim;
     float xv[32];
 #pragma unroll
@@ -217,9 +217,9 @@ __device__ __forceinline__ float load_split_rows(SplitOps& ops, const QuantArgs&
 template <bool F16>
 __device__ __forceinline__ void rotate_tokens(float (&out)[kDim], const QuantArgs& a, const void* src,
                                               const _Float16* pih, const _Float16* pil, int li, int b, int h,
-                                              int j0, int lane, bool rope) {
+                                              int j0, int Tb, int lane, bool rope) {
   SplitOps ops;
-  const float sc = load_split_rows<F16>(ops, a, src, li, b, h, j0, lane, rope);
+  const float sc = load_split_rows<F16>(ops, a, src, li, b, h, j0, Tb, lane, rope);
   f32x16 acc[2][2];
   split_products(ops, pih, pil, lane, acc);
   to_lane_per_token(acc, out);
@@ -405,7 +405,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   __syncthreads();
 
   const int j0 = blockIdx.x * 256 + wave * kTile;
-  if (j0 >= a.T) return;                  // wave-uniform; no barrier follows
+  // the sequence's tokens: all T, or its own count in a ragged call
+  const int Tb = a.tokens ? min(max(a.tokens[b], 0), a.T) : a.T;
+  if (j0 >= Tb) return;                   // wave-uniform; no barrier follows
   // a (layer, head) whose K or V table is not strictly ascending is not written
   if (!levels_ascending(Lk) || !levels_ascending(Lv)) return;
   const int64_t sbase = a.slot0[b];
@@ -421,7 +423,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   auto ok_of = [&](int jl) {
     const int64_t sl = sbase + jl;
     const int ps = pbase + jl;
-    return jl < a.T && sl >= 0 && sl < a.slots && (rotated || (ps >= 0 && ps < a.rope_positions));
+    return jl < Tb && sl >= 0 && sl < a.slots && (rotated || (ps >= 0 && ps < a.rope_positions));
   };
   auto row_of = [&](int jl) { return ((((int64_t)li * a.B + b) * a.T + jl) * a.H + h) * kDim; };
 
@@ -437,7 +439,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
 #pragma unroll
     for (int i = 0; i < kDim; ++i) x[i] = okl ? load_in(a.k, row + i, false) : 0.0f;
   } else {
-    rotate_tokens<F16>(x, a, a.k, s_pih, s_pil, li, b, h, j0, lane, true);
+    rotate_tokens<F16>(x, a, a.k, s_pih, s_pil, li, b, h, j0, Tb, lane, true);
   }
   uint32_t kw[8];
   const QuantOut qk = quantize_lane<true>(x, Lk, s_lev[0], nullptr, paper ? 2 : 3, kw);
@@ -468,7 +470,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   // are not hoisted above the key's stores (registers, occupancy).
   asm volatile("" ::: "memory");
   if (!rotated && (a.flags & kVRotate)) {
-    rotate_tokens<F16>(x, a, a.v, s_pih, s_pil, li, b, h, j0, lane, false);
+    rotate_tokens<F16>(x, a, a.v, s_pih, s_pil, li, b, h, j0, Tb, lane, false);
   } else {
     const int jl = j0 + lane;
     const bool okl = ok_of(jl);
@@ -598,8 +600,10 @@ __global__ __launch_bounds__(128) void quantize_vectors_kernel(QuantArgs a, uint
   if (any_proj) load_slice(a.qjl_s, s_sl, threadIdx.x);
   const int64_t slot = a.slot0[b] + j;
   const int pos = a.pos0[b] + (int)j;
+  const int Tb = a.tokens ? min(max(a.tokens[b], 0), a.T) : a.T;
   // block-uniform exits (before any barrier); a (layer, head) whose K or V
   // table is not strictly ascending is not written
+  if ((int)j >= Tb) return;               // beyond the sequence's tokens (a ragged call)
   if (slot < 0 || slot >= a.slots) return;
   if (!levels_ascending(L) || !levels_ascending(Lo)) return;
   if (!rotated && (pos < 0 || pos >= a.rope_positions)) return;

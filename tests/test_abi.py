@@ -37,7 +37,8 @@ def _defines():
 
 def test_header_declares_the_entry_points():
     assert _declared_functions() == sorted([
-        "tq_cache_bytes", "tq_rope_table", "tq_quantize_pack", "tq_decode_attend", "tq_decode_step",
+        "tq_cache_bytes", "tq_rope_table", "tq_quantize_pack", "tq_quantize_pack_ragged",
+        "tq_decode_attend", "tq_decode_step",
         "tq_dequantize", "tq_decode_workspace_bytes", "tq_calibrate_rotation", "tq_calibrate_lut",
         "tq_calibrate_ebar", "tq_set_step_wait_limit", "tq_decode_attend_noalloc", "tq_read_probe",
         "tq_last_error", "tq_version"])
@@ -149,6 +150,22 @@ def test_quantize_argument_checks():
     assert _quantize(_params(), _cache(), T=0) == 0
     assert _quantize(_params(), _cache(), nlayers=0) == 0
     assert tq.last_error() == ""
+
+
+def test_quantize_ragged_argument_checks():
+    L = tq._load()
+    P = ctypes.c_void_p
+    p, c = _params(), _cache()
+
+    def call(tokens, B=2, T=4, ptrs=FAKE):
+        return L.tq_quantize_pack_ragged(ctypes.byref(p), ctypes.byref(c), P(FAKE), P(FAKE), B, T,
+                                         P(tokens) if tokens else None, 0, 1, P(ptrs), P(ptrs), P(ptrs),
+                                         P(ptrs), P(ptrs), P(ptrs), None, None)
+    assert call(None) == -1 and "seq_tokens" in tq.last_error()
+    assert call(FAKE, B=-1) == -1
+    assert call(FAKE, ptrs=0) == -1
+    # nothing to do is success, with nothing launched (seq_tokens may then be NULL)
+    assert call(None, T=0) == 0 and tq.last_error() == ""
 
 
 def test_decode_argument_checks():
