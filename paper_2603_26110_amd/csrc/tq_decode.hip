@@ -931,14 +931,24 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 void decode_plan(int units, int max_len, int* waves, int* nsplit, int* split_tiles) {
   const int ntiles = max_len > 0 ? (max_len + 63) / 64 : 1;
   const int w = ntiles >= 12 ? 8 : 4;
-  // One block per unit when there are enough units to occupy every CU
-  // (a cross-block merge costs more than it balances); otherwise split the
-  // tiles so that each wave still gets at least one tile.
-  const int target_blocks = 256;
-  int ns = (target_blocks + units - 1) / units;
-  const int max_ns = (ntiles + w - 1) / w;
-  if (ns > max_ns) ns = max_ns;
-  if (ns < 1) ns = 1;
+  // A unit's tiles are split over several blocks only where that shortens
+  // the longest block: each wave's tiles are serial round trips (about
+  // 1.6 us each at low load), and a split adds a merge through the workspace
+  // (about 2 us), with the blocks of all splits fitting one pass over the
+  // 256 compute units. Costs in 0.1 us; the last token is scored apart from
+  // the tiles, so a sequence of 64 k + 1 tokens has k tiles to split.
+  constexpr int kRound = 16, kMerge = 20, kBlocks = 256;
+  const int main_tiles = max_len > 1 ? (max_len - 1 + 63) / 64 : 1;
+  const int max_ns = (ntiles + w - 1) / w;   // every wave keeps a tile
+  auto rounds = [&](int ns) {
+    const int per = (main_tiles + ns - 1) / ns;
+    return (per + w - 1) / w;
+  };
+  int ns = 1, best = rounds(1) * kRound;
+  for (int c = 2; c <= max_ns && (int64_t)units * c <= kBlocks; ++c) {
+    const int cost = rounds(c) * kRound + kMerge;
+    if (cost < best) { best = cost; ns = c; }
+  }
   int st = (ntiles + ns - 1) / ns;
   if (st > ntiles) st = ntiles;
   *waves = w;

@@ -201,6 +201,15 @@ def test_decode_flags(flags):
     _decode_check(case, _oracle_cache(case, 2, 4), [300, 310], [0, 384], [300, 257], 320)
 
 
+@pytest.mark.parametrize("flags", [tq.V_ROTATE | tq.V_QJL, tq.QJL_PAPER | tq.V_QJL | tq.V_ROTATE, 0])
+def test_decode_flags_split_k(flags):
+    # max_len 2112 plans splits of 7 tiles for these 16 units; 1100 and 700
+    # tokens span 3 and 2 of them, so the partials (with the V sign sums of
+    # TQ_V_QJL) go through the workspace merge
+    case = Case(24, 2, 4, 2, 1100, io="f16", flags=flags, slots=2 * 2112, slot0=[0, 2112])
+    _decode_check(case, _oracle_cache(case, 2, 4), [1100, 1110], [0, 2112], [1100, 700], 2112)
+
+
 @pytest.mark.parametrize("lens", [[1], [63], [64], [65], [0], [1024], [1025]])
 def test_decode_lengths(lens):
     n = max(lens)
