@@ -310,11 +310,11 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   __builtin_amdgcn_s_setprio(3);
   constexpr int NT = WAVES * 64;
   constexpr int TAM = 2048 / NT;           // pair-table entries per thread
-  constexpr int TBM = 512 / NT;            // groups of 4 sign-table entries per thread
+  constexpr int TBM = (512 + NT - 1) / NT; // groups of 4 sign-table entries per thread (512 groups)
   constexpr int COLS = kDim / WAVES;       // rows of Pi per thread in the epilogue
   // tiles in flight per wave: with 8 waves one (more only queue ahead of
   // the Pi copies of blocks that start later on the compute unit)
-  constexpr int DEPTH = WAVES == 8 ? 1 : 2;
+  constexpr int DEPTH = WAVES >= 8 ? 1 : 2;
   constexpr int MCH = 1024 / NT;           // 16-byte chunks of a 64 x 64 matrix per thread
   constexpr int NB = 2;                    // read batch of the append's row products
   __shared__ __attribute__((aligned(16))) float s_pi[kDim * kDim];   // Pi (Swz16)
@@ -500,6 +500,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
   for (int r0 = 0; r0 < kDim; r0 += NT / 8) {
     const int r = r0 + prow;
+    if (r >= kDim) break;                  // (16 waves: waves 8..15 have no row)
     const float4* m4 = reinterpret_cast<const float4*>(s_pi);
     const float4* x4 = reinterpret_cast<const float4*>(s_vec[0]);
     const float4 ma = m4[Swz16::chunk(r, 2 * pc)], mb = m4[Swz16::chunk(r, 2 * pc + 1)];
@@ -517,6 +518,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
   for (int r0 = 0; r0 < kDim; r0 += NT / 8) {
     const int r = r0 + prow;
+    if (r >= kDim) break;
     float acc = s_vec[1][r];
     if (use_s) {
       const float4* m4 = reinterpret_cast<const float4*>(s_ws);
@@ -549,6 +551,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
     for (int m = 0; m < TBM; ++m) {
       const int e = t + NT * m, k = e & 63, w = wave + WAVES * m;
+      if (e >= 512) break;
       const float4 ulo = reinterpret_cast<const float4*>(s_vec[2])[2 * w];
       const float4 uhi = reinterpret_cast<const float4*>(s_vec[2])[2 * w + 1];
       const float u[8] = {ulo.x, ulo.y, ulo.z, ulo.w, uhi.x, uhi.y, uhi.z, uhi.w};
@@ -930,28 +933,31 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 
 void decode_plan(int units, int max_len, int* waves, int* nsplit, int* split_tiles) {
   const int ntiles = max_len > 0 ? (max_len + 63) / 64 : 1;
-  const int w = ntiles >= 12 ? 8 : 4;
-  // A unit's tiles are split over several blocks only where that shortens
-  // the longest block: each wave's tiles are serial round trips (about
-  // 1.6 us each at low load), and a split adds a merge through the workspace
-  // (about 2 us), with the blocks of all splits fitting one pass over the
-  // 256 compute units. Costs in 0.1 us; the last token is scored apart from
-  // the tiles, so a sequence of 64 k + 1 tokens has k tiles to split.
+  // A unit's tiles are split over several blocks, and a block takes 16 waves
+  // rather than 8, only where that shortens the longest block: each wave's
+  // tiles are serial round trips (about 1.6 us each at low load), and a split
+  // adds a merge through the workspace (about 2 us). The blocks of all
+  // splits must fit one pass over the 256 compute units (with 16 waves a
+  // block fills a compute unit's wave slots). Costs in 0.1 us; the last
+  // token is scored apart from the tiles, so a sequence of 64 k + 1 tokens
+  // has k tiles to split.
   constexpr int kRound = 16, kMerge = 20, kBlocks = 256;
   const int main_tiles = max_len > 1 ? (max_len - 1 + 63) / 64 : 1;
-  const int max_ns = (ntiles + w - 1) / w;   // every wave keeps a tile
-  auto rounds = [&](int ns) {
-    const int per = (main_tiles + ns - 1) / ns;
-    return (per + w - 1) / w;
-  };
-  int ns = 1, best = rounds(1) * kRound;
-  for (int c = 2; c <= max_ns && (int64_t)units * c <= kBlocks; ++c) {
-    const int cost = rounds(c) * kRound + kMerge;
-    if (cost < best) { best = cost; ns = c; }
+  int best = -1, bw = ntiles >= 12 ? 8 : 4, bns = 1;
+  for (const int w : {4, 8, 16}) {
+    if ((w == 4) != (ntiles < 12)) continue;     // 4 waves for short sequences only
+    if (w == 16 && units > kBlocks) continue;
+    const int max_ns = (ntiles + w - 1) / w;     // every wave keeps a tile
+    for (int c = 1; c <= max_ns; ++c) {
+      if (c > 1 && (int64_t)units * c > kBlocks) break;
+      const int per = (main_tiles + c - 1) / c;
+      const int cost = (per + w - 1) / w * kRound + (c > 1 ? kMerge : 0);
+      if (best < 0 || cost < best) { best = cost; bw = w; bns = c; }
+    }
   }
-  int st = (ntiles + ns - 1) / ns;
+  int st = (ntiles + bns - 1) / bns;
   if (st > ntiles) st = ntiles;
-  *waves = w;
+  *waves = bw;
   *split_tiles = st;
   *nsplit = (ntiles + st - 1) / st;
 }
@@ -962,7 +968,12 @@ hipError_t launch_decode(const DecodeArgs& a, int waves, hipStream_t st) {
   const int64_t per_xcd = (total + kXcds - 1) / kXcds;
   const int64_t blocks = per_xcd * kXcds;
   const bool vq = (a.flags & kVQjl) != 0;
-  if (waves == 8) {
+  if (waves == 16) {
+    if (vq)
+      hipLaunchKernelGGL((decode_kernel<16, true>), dim3((unsigned)blocks), dim3(1024), 0, st, a, (int)total, (int)per_xcd);
+    else
+      hipLaunchKernelGGL((decode_kernel<16, false>), dim3((unsigned)blocks), dim3(1024), 0, st, a, (int)total, (int)per_xcd);
+  } else if (waves == 8) {
     if (vq)
       hipLaunchKernelGGL((decode_kernel<8, true>), dim3((unsigned)blocks), dim3(512), 0, st, a, (int)total, (int)per_xcd);
     else

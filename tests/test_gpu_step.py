@@ -149,26 +149,27 @@ def test_steps_match_oracle():
     assert_agree_up_to_threshold_rounding(case, got, ref, 1, T + steps, H, tokens=range(T, T + steps))
 
 
-@pytest.mark.parametrize("T", [768, 767, 0])
+@pytest.mark.parametrize("T", [1088, 1087, 0])
 def test_step_new_token_alone_in_its_split(T):
-    # 20 units with max_len 1088 split the tiles 6 per block (0-5, 6-11,
-    # 12-16). With 768 cached tokens the new token (index 768) starts tile
-    # 12: the last split holds no cached token, only the new one, which its
-    # block scores apart from the tiles. With 767 the new token shares tile
-    # 11 with cached ones; with 0 it is the only token.
-    L, H = 1, 20
-    case = Case(20263, L, H, 1, T + 1, io="f16", slots=1088, slot0=[0])
-    cache = tq.Cache(L, H, 1088)
+    # 20 units with max_len 8193 split the tiles 17 per block (0-16, 17-33,
+    # ...). With 1088 cached tokens the new token (index 1088) starts tile
+    # 17: the second split holds no cached token, only the new one, which its
+    # block scores apart from the tiles. With 1087 the new token shares tile
+    # 16 with cached ones; with 0 it is the only token.
+    L, H, slots = 1, 20, 8256
+    case = Case(20263, L, H, 1, T + 1, io="f16", slots=slots, slot0=[0])
+    assert tq.decode_workspace_bytes(case.params(), 1, L, 8193) > 0     # the plan splits
+    cache = tq.Cache(L, H, slots)
     _prefill(case, cache, [T], [0])
-    oc = oracle.Cache(L, H, 1088)
+    oc = oracle.Cache(L, H, slots)
     if T:
         case.oracle_quantize(oc, k=case.k[:, :, :T], v=case.v[:, :, :T])
     flags = case.flags | tq.OUT_FP32
     k = case.t("k")[:, :, T].contiguous()
     v = case.t("v")[:, :, T].contiguous()
     two = _clone(cache)
-    out = _step(case, cache, k, v, [T], [0], [T], 1088, flags)
-    out_two = _two_calls(case, two, k, v, [T], [0], [T], 1088, flags)
+    out = _step(case, cache, k, v, [T], [0], [T], 8193, flags)
+    out_two = _two_calls(case, two, k, v, [T], [0], [T], 8193, flags)
     torch.cuda.synchronize()
     assert _same_cache(cache, two)
     assert torch.equal(out, out_two)
