@@ -500,7 +500,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
   for (int r0 = 0; r0 < kDim; r0 += NT / 8) {
     const int r = r0 + prow;
-    if (r >= kDim) break;                  // (16 waves: waves 8..15 have no row)
+    if (NT > 512 && r >= kDim) break;      // (16 waves: waves 8..15 have no row)
     const float4* m4 = reinterpret_cast<const float4*>(s_pi);
     const float4* x4 = reinterpret_cast<const float4*>(s_vec[0]);
     const float4 ma = m4[Swz16::chunk(r, 2 * pc)], mb = m4[Swz16::chunk(r, 2 * pc + 1)];
@@ -518,7 +518,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
   for (int r0 = 0; r0 < kDim; r0 += NT / 8) {
     const int r = r0 + prow;
-    if (r >= kDim) break;
+    if (NT > 512 && r >= kDim) break;
     float acc = s_vec[1][r];
     if (use_s) {
       const float4* m4 = reinterpret_cast<const float4*>(s_ws);
@@ -551,7 +551,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
 #pragma unroll
     for (int m = 0; m < TBM; ++m) {
       const int e = t + NT * m, k = e & 63, w = wave + WAVES * m;
-      if (e >= 512) break;
+      if (NT > 512 && e >= 512) break;
       const float4 ulo = reinterpret_cast<const float4*>(s_vec[2])[2 * w];
       const float4 uhi = reinterpret_cast<const float4*>(s_vec[2])[2 * w + 1];
       const float u[8] = {ulo.x, ulo.y, ulo.z, ulo.w, uhi.x, uhi.y, uhi.z, uhi.w};
