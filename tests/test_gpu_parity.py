@@ -210,6 +210,18 @@ def test_decode_flags_split_k(flags):
     _decode_check(case, _oracle_cache(case, 2, 4), [1100, 1110], [0, 2112], [1100, 700], 2112)
 
 
+@pytest.mark.parametrize("flags", [tq.V_ROTATE | tq.V_QJL, tq.QJL_PAPER | tq.V_QJL | tq.V_ROTATE, tq.V_ROTATE])
+def test_decode_16_wave_blocks(flags):
+    # Few units leave compute units free, so the plan takes 16-wave blocks:
+    # 16 units of up to 1025 tokens, one block each (one tile per wave) ...
+    case = Case(25, 2, 4, 2, 1025, io="f16", flags=flags, slots=2 * 1088, slot0=[0, 1088])
+    _decode_check(case, _oracle_cache(case, 2, 4), [1025, 1030], [0, 1088], [1025, 700], 1025)
+    # ... and 20 units with max_len 8193, split 17 tiles per block: 3000
+    # tokens span three blocks, merged through the workspace
+    case = Case(26, 1, 20, 1, 3000, io="f16", flags=flags, slots=8256, slot0=[0], positions=4096)
+    _decode_check(case, _oracle_cache(case, 1, 20), [3000], [0], [3000], 8193)
+
+
 @pytest.mark.parametrize("lens", [[1], [63], [64], [65], [0], [1024], [1025]])
 def test_decode_lengths(lens):
     n = max(lens)
