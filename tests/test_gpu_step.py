@@ -112,12 +112,14 @@ def test_step_equals_append_then_attend_split_sequence():
     assert torch.equal(out_a, out_b)
 
 
-def test_steps_match_oracle():
+@pytest.mark.parametrize("flags", [tq.V_ROTATE, tq.V_ROTATE | tq.V_QJL, tq.QJL_PAPER | tq.V_QJL | tq.V_ROTATE])
+def test_steps_match_oracle(flags):
     # one layer of 20 heads: prefill 1024 tokens, then 6 decode steps, end to
     # end on both sides: the GPU steps on its cache, the oracle quantizes the
-    # same tokens into its own cache and attends there
+    # same tokens into its own cache and attends there (20 units leave
+    # compute units free: 16-wave blocks)
     L, H, T, steps = 1, 20, 1024, 6
-    case = Case(20262, L, H, 1, T + steps, io="f16", slots=1088, slot0=[0])
+    case = Case(20262, L, H, 1, T + steps, io="f16", flags=flags, slots=1088, slot0=[0])
     cache = tq.Cache(L, H, 1088)
     _prefill(case, cache, [T], [0])
     oc = oracle.Cache(L, H, 1088)
