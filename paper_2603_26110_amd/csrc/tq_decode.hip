@@ -37,7 +37,12 @@
 //             raised only when a tile max exceeds it by more than 2^8.
 //             Values are accumulated one lane per dimension from the
 //             dimension-major V tile; a tile's token weights reach the lanes
-//             through DPP row broadcasts. One tile per wave is in flight (two with 4 waves).
+//             through DPP row broadcasts. One tile per wave is in flight
+//             (two with 4 waves).
+//   blocks    WAVES = 8 for most launches; 16 where the units leave compute
+//             units free (one tile round per wave instead of two), 4 for
+//             sequences under 12 tiles; decode_plan picks the shape and the
+//             splits.
 //   merge     waves merge through LDS; splits of a unit merge through a
 //             workspace of (m, l, o) partials written and read with
 //             agent-scope atomics: the last split to finish (atomic counter)
@@ -312,7 +317,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
   constexpr int TAM = 2048 / NT;           // pair-table entries per thread
   constexpr int TBM = (512 + NT - 1) / NT; // groups of 4 sign-table entries per thread (512 groups)
   constexpr int COLS = kDim / WAVES;       // rows of Pi per thread in the epilogue
-  // tiles in flight per wave: with 8 waves one (more only queue ahead of
+  // tiles in flight per wave: with 8 or 16 waves one (more only queue ahead of
   // the Pi copies of blocks that start later on the compute unit)
   constexpr int DEPTH = WAVES >= 8 ? 1 : 2;
   constexpr int MCH = 1024 / NT;           // 16-byte chunks of a 64 x 64 matrix per thread
@@ -496,7 +501,7 @@ void decode_kernel(DecodeArgs a, int total_work, int per_xcd) {
     s_vec[0][lane] = rope_wave(xin, cs, half, lane);
   }
   lds_barrier();
-  const int prow = t >> 3, pc = t & 7;     // NT = 512: rows 0..63 (WAVES == 8); NT = 256: two passes
+  const int prow = t >> 3, pc = t & 7;     // NT = 512: rows 0..63; NT = 256: two passes; NT = 1024: waves 8..15 idle
 #pragma unroll
   for (int r0 = 0; r0 < kDim; r0 += NT / 8) {
     const int r = r0 + prow;
