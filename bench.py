@@ -24,7 +24,7 @@ dequantize-then-attend path and plain fp16 attention for context.
 Prints one JSON line.
     python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extra]
     python bench.py --workload esm2-650m-ragged-b64     (one batched workload alone)
-    python bench.py --only prefill|dequant --steps K     (eager launches, for counters)
+    python bench.py --only prefill|dequant|lengths --steps K     (eager launches, for counters)
 """
 from __future__ import annotations
 
@@ -63,9 +63,10 @@ def parse():
     ap.add_argument("--eager", action="store_true",
                     help="launch the K timed steps one by one instead of as one HIP graph "
                          "(for counter collection)")
-    ap.add_argument("--only", choices=("prefill", "dequant"), default=None,
+    ap.add_argument("--only", choices=("prefill", "dequant", "lengths"), default=None,
                     help="run only K eager launches of the prefill quantizer or of the dequantize "
-                         "baseline on the headline shape (for counter collection)")
+                         "baseline on the headline shape, or (lengths) of decode_attend and "
+                         "decode_step over 1, 513 and 1025 tokens (for counter collection)")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the ragged-batch and ESM-2 3B decode lines")
     ap.add_argument("--replays", type=int, default=10,
@@ -671,8 +672,36 @@ def only_kernel(torch, tq, which, K, params, reps, base_cache, t_, k_all, v_all,
                 lut_d, S_d, zero_i32, zero_i64):
     """K eager launches of one kernel on the headline shape, for counter
     collection: the prefill quantizer (tq_quantize_pack of the T cached
-    tokens of every unit) or the dequantize baseline (tq_dequantize of the
-    n_ctx tokens of every unit)."""
+    tokens of every unit), the dequantize baseline (tq_dequantize of the
+    n_ctx tokens of every unit), or (lengths) the decode kernel over 1, 513
+    and n_ctx tokens of every unit, first as attends (K launches per length)
+    and then as steps (K per length; a step over n tokens appends token n - 1
+    of replica 0's cache). The lengths separate a unit's fixed work (no
+    tile: only the last token), one tile per wave (8 tiles) and two."""
+    if which == "lengths":
+        lens = [1, 513, n_ctx]
+        times = {}
+        d = reps[0]
+        for mode in ("attend", "step"):
+            for n in lens:
+                qpos = torch.tensor([n - 1], dtype=torch.int32, device="cuda")
+                slen = torch.tensor([n if mode == "attend" else n - 1], dtype=torch.int32, device="cuda")
+                ea, eb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                for k in range(K + 1):
+                    if k == 1:
+                        ea.record()
+                    if mode == "attend":
+                        tq.decode_attend(params, d["cache"], d["q"], qpos, zero_i64, slen, n_ctx, d["pi"], lut_d,
+                                         lut_d, S_d, out=d["out"])
+                    else:
+                        tq.decode_step(params, d["cache"], d["q"], d["k1"], d["v1"], qpos, zero_i64, slen, n_ctx,
+                                       d["pi"], lut_d, lut_d, S_d, out=d["out"])
+                eb.record()
+                torch.cuda.synchronize()
+                times[f"{mode}_{n}"] = round(ea.elapsed_time(eb) / max(K, 1), 5)
+        print(json.dumps({"only": which, "launches_per_case": K + 1, "order": list(times),
+                          "eager_ms_per_launch": times}))
+        return
     if which == "prefill":
         pf_cache = tq.Cache(L, H, slots, device="cuda")
         k_pf, v_pf = t_(k_all[:, :, :T]), t_(v_all[:, :, :T])
