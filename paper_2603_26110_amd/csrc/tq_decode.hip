@@ -141,14 +141,17 @@ struct TileRegs {
   uint2 sc;
 };
 
+// A tile's loads in the order they are used: the key planes, then the scalars
+// (the score needs n_k and g_k), then the value planes, so that the score's
+// wait does not include the value planes.
 __device__ __forceinline__ void load_tile(TileRegs& r, const uint8_t* kreg, const uint8_t* vreg,
                                           const uint2* sreg, int64_t gt, int64_t s0, int tt,
                                           int lane) {
   r.k0 = *reinterpret_cast<const uint4*>(kreg + tile_half_offset(gt, 0, lane));
   r.k1 = *reinterpret_cast<const uint4*>(kreg + tile_half_offset(gt, 1, lane));
+  r.sc = sreg[s0 + (int64_t)tt * kTile + lane];
   r.v0 = *reinterpret_cast<const uint4*>(vreg + tile_half_offset(gt, 0, lane));
   r.v1 = *reinterpret_cast<const uint4*>(vreg + tile_half_offset(gt, 1, lane));
-  r.sc = sreg[s0 + (int64_t)tt * kTile + lane];
 }
 
 
