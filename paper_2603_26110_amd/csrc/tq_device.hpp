@@ -133,30 +133,34 @@ __device__ __forceinline__ float nearest_level(float u, const Levels& L, float c
 }
 
 // The index alone, #{m : u > t_m} (the same count as nearest_level's), for a
-// caller that reads the level itself from a table in LDS: each comparison
-// goes into the count at once, so no lane mask stays live across the
-// elements of a vector (64 unrolled select chains keep so many masks live
-// that they spill).
-__device__ __forceinline__ uint32_t level_index(float u, const Levels& L) {
-  // t_m < u sets VCC (false for a NaN u, like u > t_m), which the next
-  // instruction adds into the count
+// caller that reads the level itself from a table in LDS. The comparisons
+// write VCC only and each is used at once, so no lane mask stays live across
+// the elements of a vector (64 unrolled select chains keep so many masks
+// live that they spill).
+__device__ __forceinline__ uint32_t level_index(float u, const Levels& L, const float* thr_even) {
+  // The count is the length of the prefix of thresholds below u (they are
+  // non-decreasing), found in three steps: b2 = [t3 < u], b1 =
+  // [t(b2 ? 5 : 1) < u] and b0 = [t(4 b2 + 2 b1) < u], each bit added into
+  // the count by a carry (a NaN u compares false throughout, like the
+  // count). The second threshold is selected in registers (t1 and t5 as
+  // vector operands: a select that reads VCC cannot also read a scalar);
+  // the third, t(2 i) for i = 2 b2 + b1, is read from thr_even = {t0, t2, t4,
+  // t6} in LDS.
   uint32_t i;
-  asm("v_cmp_lt_f32 vcc, %1, %8\n\t"
-      "v_cndmask_b32 %0, 0, 1, vcc\n\t"
-      "v_cmp_lt_f32 vcc, %2, %8\n\t"
-      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
-      "v_cmp_lt_f32 vcc, %3, %8\n\t"
-      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
-      "v_cmp_lt_f32 vcc, %4, %8\n\t"
-      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
-      "v_cmp_lt_f32 vcc, %5, %8\n\t"
-      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
-      "v_cmp_lt_f32 vcc, %6, %8\n\t"
-      "v_addc_co_u32 %0, vcc, 0, %0, vcc\n\t"
-      "v_cmp_lt_f32 vcc, %7, %8\n\t"
-      "v_addc_co_u32 %0, vcc, 0, %0, vcc"
-      : "=&v"(i)
-      : "s"(L.t0), "s"(L.t1), "s"(L.t2), "s"(L.t3), "s"(L.t4), "s"(L.t5), "s"(L.t6), "v"(u)
+  float ta;
+  asm("v_cmp_lt_f32 vcc, %2, %5\n\t"
+      "v_cndmask_b32_e64 %0, 0, 1, vcc\n\t"
+      "v_cndmask_b32 %1, %3, %4, vcc\n\t"
+      "v_cmp_lt_f32 vcc, %1, %5\n\t"
+      "v_addc_co_u32 %0, vcc, %0, %0, vcc"
+      : "=&v"(i), "=&v"(ta)
+      : "s"(L.t3), "v"(L.t1), "v"(L.t5), "v"(u)
+      : "vcc");
+  const float tb = thr_even[i];
+  asm("v_cmp_lt_f32 vcc, %1, %2\n\t"
+      "v_addc_co_u32 %0, vcc, %0, %0, vcc"
+      : "+v"(i)
+      : "v"(tb), "v"(u)
       : "vcc");
   return i;
 }
@@ -168,7 +172,7 @@ struct QuantOut {
 
 template <bool KEY_WORDS>
 __device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Levels& L, const float* lev,
-                                                  const float* S, int sign_mode,
+                                                  const float* thr_even, const float* S, int sign_mode,
                                                   uint32_t (&words)[8]) {
   float s = 0.0f;
 #pragma unroll
@@ -180,7 +184,7 @@ __device__ __forceinline__ QuantOut quantize_lane(float (&xh)[kDim], const Level
 #pragma unroll
   for (int i = 0; i < kDim; ++i) {
     const float u = xh[i] * inv;
-    const uint32_t idx = level_index(u, L);
+    const uint32_t idx = level_index(u, L, thr_even);
     const float lv = lev[idx];   // the level c[idx], from the table in LDS
     words[i >> 3] |= idx << ((KEY_WORDS ? 3 : 4) * (i & 7));
     xh[i] = u - lv;   // residual r_i

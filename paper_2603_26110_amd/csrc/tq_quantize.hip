@@ -349,6 +349,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   __shared__ float s_Sn[kDim];                                               // ||sigma_i S_i||
   __shared__ uint32_t s_vt[4][kDim * 8];
   __shared__ float s_lev[2][8];                                              // K and V levels
+  __shared__ float s_thr[2][4];                                              // their t0, t2, t4, t6
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
 
   const int h = blockIdx.y % a.H, b = blockIdx.y / a.H, li = blockIdx.z;
@@ -402,6 +403,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
   }
   const Levels Lk = load_levels(a.lut_k + lh * 8);
   const Levels Lv = load_levels(a.lut_v + lh * 8);
+  if (threadIdx.x == 0) {
+    s_thr[0][0] = Lk.t0; s_thr[0][1] = Lk.t2; s_thr[0][2] = Lk.t4; s_thr[0][3] = Lk.t6;
+    s_thr[1][0] = Lv.t0; s_thr[1][1] = Lv.t2; s_thr[1][2] = Lv.t4; s_thr[1][3] = Lv.t6;
+  }
   __syncthreads();
 
   const int j0 = blockIdx.x * 256 + wave * kTile;
@@ -442,7 +447,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
     rotate_tokens<F16>(x, a, a.k, s_pih, s_pil, li, b, h, j0, Tb, lane, true);
   }
   uint32_t kw[8];
-  const QuantOut qk = quantize_lane<true>(x, Lk, s_lev[0], nullptr, paper ? 2 : 3, kw);
+  const QuantOut qk = quantize_lane<true>(x, Lk, s_lev[0], s_thr[0], nullptr, paper ? 2 : 3, kw);
   if (!paper) {
     // the key words wait in this wave's transpose buffer while the signs are
     // computed (registers)
@@ -479,7 +484,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void q
     for (int i = 0; i < kDim; ++i) x[i] = okl ? load_in(a.v, row + i, F16) : 0.0f;
   }
   uint32_t vw[8];
-  const QuantOut qv = quantize_lane<false>(x, Lv, s_lev[1], nullptr, (VQJL && !paper) ? 3 : vsign, vw);
+  const QuantOut qv = quantize_lane<false>(x, Lv, s_lev[1], s_thr[1], nullptr, (VQJL && !paper) ? 3 : vsign, vw);
   // V is stored dimension-major: transpose the wave's 64 x 64 nibbles through
   // its LDS buffer (token-major words in, one dimension per lane out). The
   // words go there first; the projected signs of the value residual, where
