@@ -336,10 +336,11 @@ __device__ __forceinline__ uint64_t projected_signs(float (&x)[kDim], float g, c
 // 64 x 8 word buffer per wave for the V transpose.
 // Three waves per SIMD (168 registers, no spills for the default flags: the
 // key words and the value words wait in LDS while their signs are computed,
-// per-lane slot facts are recomputed where used, a level's index is counted
-// by compare-and-carry). Asking the compiler for four waves per SIMD gives
-// 232 registers (two waves) instead: the two rotations' and the projection's
-// 64-value results and their operands do not fit in 128.
+// per-lane slot facts are recomputed where used, a level's index is found by
+// a three-step search whose comparisons each write VCC only). Asking the
+// compiler for four waves per SIMD gives 232 registers (two waves) instead:
+// the two rotations' and the projection's 64-value results and their
+// operands do not fit in 128.
 template <bool F16, bool VQJL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void quantize_tiles_kernel(QuantArgs a) {
   __shared__ __attribute__((aligned(16))) _Float16 s_pih[kDim * kHPitch];   // Pi, fp16 parts
