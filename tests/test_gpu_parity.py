@@ -88,6 +88,47 @@ def test_quantize_bit_exact_on_rotated_inputs(T, B, slot0, flags):
     assert oc.s.any()
 
 
+@pytest.mark.parametrize("T,flags", [
+    (128, tq.V_ROTATE),                 # tile kernel
+    (128, tq.QJL_PAPER | tq.V_QJL),
+    (16, tq.V_ROTATE | tq.V_QJL),       # wave-per-vector kernel
+])
+def test_quantize_bit_exact_at_thresholds(T, flags):
+    """Coordinates exactly on the decision thresholds. The levels are the
+    half-integers -3.5 .. 3.5, so the thresholds are the integers -3 .. 3;
+    each vector holds the values 0, +-1, +-2, +-3 with squares summing to
+    64, times a power of two, so its norm is exactly 8 times that power and u
+    equals the unscaled vector exactly. The index counts the thresholds
+    strictly below u (Eq. 5 with ties to the lower level), so every such
+    coordinate must land on the lower level, on both kernels."""
+    L, H, B = 1, 2, 1
+    lut = np.arange(-3.5, 4.0, 1.0, dtype=np.float32)
+    case = Case(13, L, H, B, T, io="f32", flags=flags | tq.INPUT_ROTATED, slots=256, slot0=[64],
+                lut_k=lut, lut_v=lut)
+    g = np.random.default_rng(5)
+    base = np.array([3, -3, 2, -2, 1, -1, 3, -3, 3, -3] + [0] * 54, np.float32)
+    assert float(np.sum(base.astype(np.float64) ** 2)) == 64.0
+
+    def vectors():
+        out = np.empty((L, B, T, H, 64), np.float32)
+        for idx in np.ndindex(L, B, T, H):
+            sgn = np.where(g.random(64) < 0.5, -1.0, 1.0).astype(np.float32)
+            out[idx] = g.permutation(base) * sgn * np.float32(2.0 ** int(g.integers(-4, 5)))
+        return out
+
+    kh, vh = vectors(), vectors()
+    cache = tq.Cache(L, H, 256)
+    case.gpu_quantize(cache, k=torch.from_numpy(kh).cuda(), v=torch.from_numpy(vh).cuda())
+    torch.cuda.synchronize()
+    oc = oracle.Cache(L, H, 256)
+    case.oracle_quantize(oc, k=kh, v=vh)
+    got = device_bytes(cache)
+    np.testing.assert_array_equal(got.s, oc.s)
+    np.testing.assert_array_equal(got.k, oc.k)
+    np.testing.assert_array_equal(got.v, oc.v)
+    assert oc.k.any() and oc.v.any()
+
+
 @pytest.mark.parametrize("flags", [tq.V_ROTATE, tq.V_ROTATE | tq.V_QJL])
 def test_projected_signs_inside_the_guard_band_are_exact(flags):
     # The tile kernel takes a projected sign from its matrix-core product only
