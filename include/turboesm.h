@@ -277,9 +277,9 @@ TQ_API tq_status tq_decode_attend_noalloc(const tq_params* params, const tq_cach
  *           A sequence that would exceed max_len, its slot range or the RoPE
  *           table is not appended and gets NaN output (as does a (layer,
  *           head) whose lut_k or lut_v is not strictly ascending).
- *           The block's waves that score the new token's tile wait, bounded,
- *           for the block's own waves that append it (they wait on nothing,
- *           so the bound is never reached in practice); if the wait gives
+ *           The block's wave that scores the new token waits, bounded, for
+ *           the block's own waves that append it (they wait on nothing, so
+ *           the bound is never reached in practice); if the wait gives
  *           up, that unit's output is NaN (the appended codes are in the
  *           cache). tq_set_step_wait_limit sets the bound.
  *   max_len host bound on every seq_len[b] + 1, >= 1.
